@@ -1,0 +1,266 @@
+#!/usr/bin/env python3
+"""Throughput of the Winograd convolution hot path on one MI355X (gfx950).
+
+One step = one full layer through eq. (2) of Barabasz & Gregg (arXiv
+1905.05233): kernel transform, input transform, alpha'^2 batched matrix-core
+contraction and output transform, on seeded synthetic inputs already resident
+in HBM.  Default workload: conv3x3 stride 1 pad 1, N=8, C=K=128, H=W=56, fp32,
+F(4x4,3x3) with points {0, 1, -1, 1/2, -1/2, inf}.
+
+Prints one JSON line: direct-equivalent TFLOP/s (2 N H W C K 9 flops per
+step), per-kernel average durations (HIP events on the launch stream), the
+roofline of the dominant kernel, the rel-L2 error against fp64 direct
+convolution, and the CPU oracle's throughput on the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload cfg2] [--plan 0]
+"""
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "direct-equiv conv TFLOP/s + MFMA util/HBM GB/s; rel-L2 err vs fp64 direct"
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0, "bf16": 2500.0}
+KERNEL_NAMES = ("kernel_transform", "input_transform", "contract", "output_transform")
+KERNEL_SOURCES = {"kernel_transform": "transforms.hip", "input_transform": "transforms.hip",
+                  "contract": "contract.hip", "output_transform": "transforms.hip"}
+
+
+def algorithmic_work(wl, alpha, m):
+    """Bytes / flops each kernel must move or compute for one layer."""
+    s = 4 if wl.dtype == "f32" else 2
+    th, tw = -(-wl.H // m), -(-wl.W // m)
+    T = wl.N * th * tw
+    a2 = alpha * alpha
+    C, K = wl.C, wl.K
+    return {
+        "kernel_transform": {"bytes": 9 * C * K * s + a2 * C * K * s},
+        "input_transform": {"bytes": wl.N * wl.H * wl.W * C * s + a2 * T * C * s},
+        "contract": {"flops": 2 * a2 * T * C * K, "bytes": a2 * (T * C * s + K * C * s + T * K * 4)},
+        "output_transform": {"bytes": a2 * T * K * 4 + wl.N * wl.H * wl.W * K * s},
+        "T": T,
+    }
+
+
+def source_hash(name):
+    with open(os.path.join(ROOT, "paper_1905_05233_amd", "csrc", name), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(kernel, workload_tag):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if they
+    were taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_tag}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256_16") != source_hash(KERNEL_SOURCES[kernel]):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = [p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
+        return max(n) if n else 1
+    except Exception:
+        return 1
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="cfg2")
+    ap.add_argument("--plan", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="CPU oracle time budget (0 disables the cpu_baseline leg)")
+    ap.add_argument("--graph", action="store_true", help="replay each step from a captured HIP graph")
+    ap.add_argument("--profile-kernel", default=None, choices=KERNEL_NAMES,
+                    help="only launch this kernel, --steps times (for counter collection)")
+    a = ap.parse_args(argv)
+
+    if a.gpus != 1:
+        print(f"bench.py: this library runs on one GPU; --gpus {a.gpus} is not supported "
+              "(sharding is described in the design notes, not built)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_1905_05233_amd import _native as NAT
+    from paper_1905_05233_amd import workloads as WL
+    from paper_1905_05233_amd.winograd import Plan
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    dev = torch.device("cuda:0")
+    wl = WL.CONFIGS[a.workload]
+    ps = wl.plans[a.plan]
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[wl.dtype]
+    x32, w32 = wl.draw()
+    xd = torch.from_numpy(x32).to(tdt).to(dev)
+    wd = torch.from_numpy(w32).to(tdt).to(dev)
+    y = torch.empty((wl.N, wl.H, wl.W, wl.K), dtype=tdt, device=dev)
+    plan = Plan(ps.moduli, m=ps.m, dtype=wl.dtype, inner=ps.inner)
+    work = algorithmic_work(wl, plan.alpha, plan.m)
+    step = plan.bind_call(xd, wd, y)
+    stream = torch.cuda.current_stream()
+
+    lib = NAT.lib()
+    g = plan.geometry(wl.N, wl.H, wl.W, wl.C, wl.K)
+    a2 = plan.alpha ** 2
+    U = torch.empty((a2, wl.K, g["Cp"]), dtype=tdt, device=dev)
+    V = torch.empty((a2, g["T"], g["Cp"]), dtype=tdt, device=dev)
+    M = torch.empty((a2, g["T"], g["Kp"]), dtype=torch.float32, device=dev)
+    xt = NAT.WgTensor(ctypes.c_void_p(xd.data_ptr()), wl.N, wl.H, wl.W, wl.C)
+    wt = NAT.WgTensor(ctypes.c_void_p(wd.data_ptr()), wl.K, 3, 3, wl.C)
+    yt = NAT.WgTensor(ctypes.c_void_p(y.data_ptr()), wl.N, wl.H, wl.W, wl.K)
+    sh = ctypes.c_void_p(stream.cuda_stream)
+    stages = {
+        "kernel_transform": lambda: lib.winograd_kernel_transform(plan._h, ctypes.byref(wt),
+                                                                  ctypes.c_void_p(U.data_ptr()), sh),
+        "input_transform": lambda: lib.winograd_input_transform(plan._h, ctypes.byref(xt),
+                                                                ctypes.c_void_p(V.data_ptr()), sh),
+        "contract": lambda: lib.winograd_contract(plan._h, ctypes.c_void_p(V.data_ptr()),
+                                                  ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(M.data_ptr()),
+                                                  g["T"], wl.C, wl.K, sh),
+        "output_transform": lambda: lib.winograd_output_transform(plan._h, ctypes.c_void_p(M.data_ptr()),
+                                                                  ctypes.byref(yt), sh),
+    }
+
+    if a.profile_kernel:
+        for name in KERNEL_NAMES:       # produce valid inputs for the profiled kernel
+            NAT.check(stages[name]())
+        torch.cuda.synchronize()
+        for _ in range(a.steps):
+            NAT.check(stages[a.profile_kernel]())
+        torch.cuda.synchronize()
+        print(json.dumps({"profiled": a.profile_kernel, "launches": a.steps}))
+        return 0
+
+    # ---------------------------------------------------------- whole step
+    run = step
+    graph = None
+    if a.graph:
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        run = graph.replay
+    for _ in range(a.warmup):
+        run()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(a.steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / a.steps
+    value = wl.direct_flops / (ms_per_step * 1e-3) / 1e12
+
+    # ------------------------------------------- per-kernel event timing
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(KERNEL_NAMES) + 1)] for _ in range(a.steps)]
+    for _ in range(3):
+        for name in KERNEL_NAMES:
+            NAT.check(stages[name]())
+    torch.cuda.synchronize()
+    for it in range(a.steps):
+        ev[it][0].record(stream)
+        for k, name in enumerate(KERNEL_NAMES):
+            NAT.check(stages[name]())
+            ev[it][k + 1].record(stream)
+    torch.cuda.synchronize()
+    kernel_us = {name: 1e3 * sum(ev[it][k].elapsed_time(ev[it][k + 1]) for it in range(a.steps)) / a.steps
+                 for k, name in enumerate(KERNEL_NAMES)}
+
+    wtag = a.workload + (f"p{a.plan}" if a.plan else "")
+    kernels = {}
+    for name in KERNEL_NAMES:
+        us = kernel_us[name]
+        rec = {"avg_us": round(us, 3), "algorithmic_bytes": work[name]["bytes"],
+               "GB_s": round(work[name]["bytes"] / (us * 1e-6) / 1e9, 1)}
+        if "flops" in work[name]:
+            rec["algorithmic_flops"] = work[name]["flops"]
+            rec["TFLOP_s"] = round(work[name]["flops"] / (us * 1e-6) / 1e12, 2)
+        kernels[name] = rec
+    dom = max(KERNEL_NAMES, key=lambda n: kernel_us[n])
+    us = kernel_us[dom]
+    if dom == "contract":
+        ai = work[dom]["flops"] / work[dom]["bytes"]
+        ridge = MFMA_PEAK_TFLOPS[wl.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+        if ai >= ridge:
+            achieved = work[dom]["flops"] / (us * 1e-6) / 1e12
+            roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_PEAK_TFLOPS[wl.dtype],
+                    "unit": "TFLOP/s"}
+        else:
+            achieved = work[dom]["bytes"] / (us * 1e-6) / 1e9
+            roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    else:
+        achieved = work[dom]["bytes"] / (us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["kernel"] = dom
+    roof["traffic"] = load_traffic(dom, wtag)
+
+    # --------------------------------------------- accuracy and CPU oracle
+    step()
+    torch.cuda.synchronize()
+    y_gpu = y.float().cpu().numpy().astype(np.float64)
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s (direct-equivalent)",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"conv3x3 s1 p1 NHWC N={wl.N} C={wl.C} K={wl.K} H=W={wl.H} {wl.dtype} "
+                               f"F({ps.m}x{ps.m},3x3) moduli {{{ps.moduli}}}",
+                   "N": wl.N, "H": wl.H, "W": wl.W, "C": wl.C, "K": wl.K, "moduli": ps.moduli, "m": ps.m,
+                   "alpha": plan.alpha, "tiles": work["T"], "graph": bool(a.graph)},
+        "kernels": kernels, "roofline": roof,
+    }
+    if a.cpu_seconds > 0:
+        from oracle import conv as OC
+        from oracle import fp as OF
+        from oracle import plan as OP
+        x, w = OF.to_dtype(x32, wl.dtype), OF.to_dtype(w32, wl.dtype)
+        op = OP.build_plan(ps.moduli, n_o=ps.m, inner=ps.inner)
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            yo = OC.winograd_emulated(x, w, op, wl.dtype)
+            reps += 1
+            if time.perf_counter() - t0 >= a.cpu_seconds:
+                break
+        dt = time.perf_counter() - t0
+        y64 = OC.direct_f64(x, w)
+        err_gpu = OC.rel_l2(y_gpu, y64)
+        err_or = OC.rel_l2(yo, y64)
+        out["rel_l2"] = {"gpu_vs_fp64_direct": err_gpu, "oracle_vs_fp64_direct": err_or, "cap": wl.cap,
+                         "pass": bool(err_gpu <= min(2 * err_or, wl.cap))}
+        out["cpu_baseline"] = {"value": round(wl.direct_flops * reps / dt / 1e12, 6),
+                               "unit": "TFLOP/s (direct-equivalent)", "cores": blas_threads(), "kind": "oracle",
+                               "sample": f"{reps} full layer(s) of the same workload through the oracle's "
+                                         f"rounding-emulated Winograd (numpy; BLAS threads for the channel "
+                                         f"sums, one thread elsewhere), {dt:.1f} s"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,175 @@
+/*
+ * winograd_crt.h -- C ABI of the MI355X (gfx950) Winograd convolution library.
+ *
+ * The library computes a DNN convolution layer with 3x3 kernels (stride 1,
+ * zero padding 1, cross-correlation as in DNN frameworks) by the 2D Winograd
+ * algorithm in the matrix-exchange form of Barabasz & Gregg, "Winograd
+ * Convolution for DNNs: Beyond linear polynomials" (arXiv 1905.05233),
+ * eq. (2):
+ *
+ *     Y = A^T [ (G g G^T) (.) (B^T d B) ] A
+ *
+ * on every (m+2)x(m+2) input tile d and 3x3 kernel g, summed over input
+ * channels.  The transforms G (alpha' x 3), A (alpha' x m) and B
+ * ((m+2) x alpha') are built by the polynomial Chinese Remainder Theorem
+ * (Section 2.1, eq. (1)) from a set of moduli that may contain degree-2
+ * ("superlinear") polynomials as well as linear ones (points), following
+ * Algorithm 1 (G, A) and Algorithm 2 (B) of Section 2.2, in exact rational
+ * arithmetic on the host.
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are dense, row-major, in device memory:
+ *       x  [N][H][W][C]   (NHWC input)
+ *       w  [K][3][3][C]   (weights)
+ *       y  [N][H][W][K]   (NHWC output)
+ *     all in the plan's storage dtype (fp32, fp16 or bf16).  Every transform
+ *     runs in fp32 registers; the channel contraction accumulates in fp32 for
+ *     every dtype; results are rounded to the dtype once, when stored.
+ *   - Device pointers must be 16-byte aligned.
+ *   - Every function returns a wg_status; on error the out-parameters are left
+ *     untouched and winograd_last_error() describes the failure.  No C++
+ *     exception crosses this interface.
+ *   - Launching functions are asynchronous on the given HIP stream and never
+ *     synchronise.  A plan is immutable after creation except for its bound
+ *     workspace: do not use one plan on two streams at the same time.
+ *   - The caller owns every buffer and the stream; a plan owns only its host
+ *     tables and is released by winograd_plan_destroy().
+ */
+#ifndef WINOGRAD_CRT_H
+#define WINOGRAD_CRT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { WG_F32 = 0, WG_F16 = 1, WG_BF16 = 2 } wg_dtype;
+
+typedef enum {
+    WG_OK = 0,
+    WG_ERR_ARG = 1,          /* null pointer, bad size, misaligned pointer, parse error */
+    WG_ERR_DEGREE_SUM = 2,   /* sum of modulus degrees does not match m + r - 1 */
+    WG_ERR_NOT_COPRIME = 3,  /* two moduli share a factor (Section 2.1) */
+    WG_ERR_REDUCIBLE = 4,    /* a modulus is reducible over Q (Section 2.1) */
+    WG_ERR_UNSUPPORTED = 5,  /* r != 3, alpha' or tile beyond the kernels' range, dtype */
+    WG_ERR_OVERFLOW = 6,     /* exact rational arithmetic left the int64 range */
+    WG_ERR_WORKSPACE = 7,    /* no workspace bound, or too small */
+    WG_ERR_HIP = 8,          /* a HIP runtime call or kernel launch failed */
+    WG_ERR_INTERNAL = 9      /* the exact self-check of a built plan failed */
+} wg_status;
+
+/* An exact rational num/den (den > 0 after normalisation). */
+typedef struct { int64_t num, den; } wg_rational;
+
+/* One modulus m_i(a) of the CRT (Section 2.1).  degree 0 denotes the
+ * pseudo-point infinity of the "modified" algorithm (Section 2.1, Algorithm 1
+ * last rows); otherwise coef[0..degree] are the coefficients, lowest power
+ * first (the paper's vec() order).  Moduli are made monic by the library. */
+typedef struct { int degree; wg_rational coef[4]; } wg_modulus;
+
+/* The modulus set and the evaluation points of the inner Toom-Cook
+ * algorithm F_T-C(d x d, d x d) used for every degree-d modulus
+ * (Section 2.1, Algorithm 1 and 2).  Row order of the Winograd domain:
+ * modulus list order, 2d-1 rows per degree-d modulus in inner-point order,
+ * the pseudo-point last.  A degree-d modulus uses the first 2d-2 inner points
+ * plus infinity when inner_inf != 0, else the first 2d-1 points.  With
+ * n_inner == 0 the points 0, -1 and infinity are used (Section 3.1). */
+typedef struct {
+    int n_mod;
+    const wg_modulus* mods;
+    int n_inner;
+    const wg_rational* inner_pts;
+    int inner_inf;
+} wg_poly_set;
+
+/* A dense NHWC tensor (weights: n = K, h = w = 3, c = C). */
+typedef struct { void* data; int64_t n, h, w, c; } wg_tensor;
+
+typedef struct wg_plan_s* wg_plan;
+
+/* Build the transforms of F(m x m, r x r) from a modulus set (Algorithms 1
+ * and 2) in exact rational arithmetic, check them with the exact CRT
+ * reconstruction identity sum_xi B[k,xi] G[xi,i] A[xi,j] = [k == i+j], and
+ * round them once to fp32 (nearest, ties to even) for the kernels.
+ * Requirements: r == 3; the moduli are irreducible and pairwise coprime;
+ * sum of finite degrees == m + r - 2 with the pseudo-point, m + r - 1
+ * without; 3 <= m + 2 <= 16 and alpha' <= 16.  *out receives a new plan. */
+wg_status winograd_plan_create(const wg_poly_set* set, int m, int r, wg_dtype dtype, wg_plan* out);
+
+/* Same as winograd_plan_create with the set written as text: a comma list
+ * of points ("0", "-1/2"), polynomials in a ("a^2+1", "a^2-a+1") and "inf";
+ * inner is the inner point list, e.g. "0,-1,inf" (NULL or "" = default). */
+wg_status winograd_plan_create_str(const char* moduli, const char* inner, int m, int r,
+                                   wg_dtype dtype, wg_plan* out);
+
+/* Release a plan (NULL is ignored).  Does not free a bound workspace. */
+void winograd_plan_destroy(wg_plan plan);
+
+/* alpha' = sum over finite moduli of (2 deg - 1), plus 1 for infinity. */
+int winograd_plan_alpha(wg_plan plan);
+
+/* m, r, alpha', input tile m + r - 1 and dtype of a plan. */
+wg_status winograd_plan_info(wg_plan plan, int* m, int* r, int* alpha, int* tile_in, int* dtype);
+
+/* Exact matrix 'G' (alpha' x r), 'A' (alpha' x m) or 'B' ((m+r-1) x alpha'),
+ * row-major, into out[cap] (cap >= rows * cols). */
+wg_status winograd_plan_matrix(wg_plan plan, char which, wg_rational* out, size_t cap);
+
+/* The same matrix as the fp32 values the kernels use. */
+wg_status winograd_plan_matrix_f32(wg_plan plan, char which, float* out, size_t cap);
+
+/* Elementwise multiplications per output point, alpha'^2 / m^2 (Section 2.3,
+ * Table 1), as an exact fraction. */
+wg_status winograd_plan_ratio(wg_plan plan, int64_t* num, int64_t* den);
+
+/* Device workspace needed by winograd_conv2d for this layer shape. */
+wg_status winograd_workspace_bytes(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C,
+                                   int64_t K, size_t* bytes);
+
+/* Bind a caller-owned device workspace (256-byte aligned) to the plan; a
+ * NULL pointer unbinds.  The plan keeps the pointer, not the memory. */
+wg_status winograd_plan_set_workspace(wg_plan plan, void* dev_ptr, size_t bytes);
+
+/* y = conv3x3(x, w) by eq. (2): launches the kernel transform, the input
+ * transform, the alpha'^2 batched channel contraction and the output
+ * transform on `stream`, using the bound workspace.  x is [N][H][W][C],
+ * w is [K][3][3][C], y is [N][H][W][K]; N, H, W, C, K >= 1 (y->c = K). */
+wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
+                          hipStream_t stream);
+
+/* ---- Stage entry points (each launches one kernel of winograd_conv2d) ----
+ * Intermediate layouts, with Cp = C rounded up to a multiple of 8,
+ * Kp = K rounded up to a multiple of 8, T = N * ceil(H/m) * ceil(W/m) tiles,
+ * tile index t = (n * ceil(H/m) + ty) * ceil(W/m) + tx and Winograd-domain
+ * index xi = i * alpha' + j:
+ *   U [alpha'^2][K][Cp]  dtype, channels Cp > C are zero
+ *   V [alpha'^2][T][Cp]  dtype, channels Cp > C are zero
+ *   M [alpha'^2][T][Kp]  fp32 (columns K..Kp-1 are not written)          */
+
+/* U[xi][k][c] = (G g_kc G^T)[i][j]: eq. (2)'s kernel transform. */
+wg_status winograd_kernel_transform(wg_plan plan, const wg_tensor* w, void* U, hipStream_t stream);
+
+/* V[xi][t][c] = (B^T d_tc B)[i][j], d_tc the (m+2)^2 window of channel c whose
+ * top-left input pixel is (ty*m - 1, tx*m - 1); pixels outside x read 0. */
+wg_status winograd_input_transform(wg_plan plan, const wg_tensor* x, void* V, hipStream_t stream);
+
+/* M[xi][t][k] = sum_c V[xi][t][c] U[xi][k][c]: alpha'^2 GEMMs [T x C][C x K]
+ * on the matrix cores with fp32 accumulation (the Hadamard product of eq. (2)
+ * summed over input channels). */
+wg_status winograd_contract(wg_plan plan, const void* V, const void* U, float* M, int64_t T,
+                            int64_t C, int64_t K, hipStream_t stream);
+
+/* y[n][ty*m+o][tx*m+p][k] = (A^T M_tk A)[o][p], stored only inside H x W. */
+wg_status winograd_output_transform(wg_plan plan, const float* M, wg_tensor* y, hipStream_t stream);
+
+/* Message describing the last error of the calling thread ("" if none). */
+const char* winograd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WINOGRAD_CRT_H */

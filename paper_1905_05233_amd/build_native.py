@@ -1,0 +1,85 @@
+"""Compile the native library ``libwinograd_crt.so`` for gfx950 with hipcc.
+
+Usage: ``python -m paper_1905_05233_amd.build_native [-j JOBS]``.  Objects go
+to ``_build/`` at the repository root; the shared library is written next to
+this file, where the Python binding loads it.  Always recompiles.
+"""
+import argparse
+import os
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+BUILD = os.path.join(ROOT, "_build")
+LIB = os.path.join(PKG, "libwinograd_crt.so")
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}"]
+# device code: no packed-fp32 instructions (v_pk_*_f32) anywhere
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          "-ffp-contract=fast"]
+
+# (source, extra flags, object name)
+UNITS = [
+    ("rational.cpp", [], "rational.o"),
+    ("plan.cpp", [], "plan.o"),
+    ("api.hip", DEVICE, "api.o"),
+    ("contract.hip", DEVICE, "contract.o"),
+    ("transforms.hip", DEVICE + ["-DWG_DTYPE=0"], "transforms_f32.o"),
+    ("transforms.hip", DEVICE + ["-DWG_DTYPE=1"], "transforms_f16.o"),
+    ("transforms.hip", DEVICE + ["-DWG_DTYPE=2"], "transforms_bf16.o"),
+]
+
+
+def _run(cmd):
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    out = "\n".join(line for line in r.stdout.splitlines() if "packed-fp32-ops" not in line)
+    if r.returncode != 0:
+        raise RuntimeError(f"command failed ({r.returncode}): {' '.join(cmd)}\n{out}")
+    return out
+
+
+def compile_unit(unit):
+    src, extra, obj = unit
+    path = os.path.join(CSRC, src)
+    out = os.path.join(BUILD, obj)
+    if src.endswith(".cpp"):
+        cmd = [HIPCC, "-x", "c++"] + COMMON + ["-c", path, "-o", out]
+    else:
+        cmd = [HIPCC] + COMMON + extra + ["-c", path, "-o", out]
+    return _run(cmd)
+
+
+def build(jobs=None, verbose=False):
+    os.makedirs(BUILD, exist_ok=True)
+    jobs = jobs or min(8, os.cpu_count() or 4)
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        logs = list(ex.map(compile_unit, UNITS))
+    objs = [os.path.join(BUILD, u[2]) for u in UNITS]
+    tmp = LIB + ".tmp"
+    link = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}"] + objs + ["-o", tmp]
+    logs.append(_run(link))
+    os.replace(tmp, LIB)
+    if verbose:
+        for log in logs:
+            if log.strip():
+                print(log)
+    return LIB
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("-j", "--jobs", type=int, default=None)
+    ap.add_argument("-v", "--verbose", action="store_true")
+    a = ap.parse_args(argv)
+    print(build(a.jobs, a.verbose))
+
+
+if __name__ == "__main__":
+    sys.exit(main())

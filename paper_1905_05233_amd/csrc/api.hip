@@ -1,0 +1,352 @@
+// C ABI of the Winograd convolution library (declared in winograd_crt.h).
+//
+// Host side: plan creation (exact transforms from plan.cpp), argument and
+// workspace validation, and the four kernel launches of eq. (2)
+// (Barabasz & Gregg, arXiv 1905.05233).  No C++ exception leaves this file;
+// every failure becomes a wg_status plus a thread-local message.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "plan.hpp"
+#include "winograd_crt.h"
+
+struct wg_plan_s {
+    wg::Transforms tr;
+    int dtype = 0;
+    void* ws = nullptr;
+    size_t ws_bytes = 0;
+    wg::InputTable itab{};
+    wg::KernelTable ktab{};
+    wg::OutputTable otab{};
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+wg_status fail(wg_status s, const std::string& msg) {
+    g_last_error = msg;
+    return s;
+}
+
+wg_status from_hip(hipError_t e, const char* what) {
+    if (e == hipSuccess) return WG_OK;
+    return fail(WG_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+template <typename F>
+wg_status guarded(F&& f) {
+    try {
+        return f();
+    } catch (const wg::PlanError& e) {
+        return fail(static_cast<wg_status>(e.status), e.what());
+    } catch (const wg::OverflowError& e) {
+        return fail(WG_ERR_OVERFLOW, e.what());
+    } catch (const std::bad_alloc&) {
+        return fail(WG_ERR_INTERNAL, "host out of memory");
+    } catch (const std::exception& e) {
+        return fail(WG_ERR_INTERNAL, e.what());
+    } catch (...) {
+        return fail(WG_ERR_INTERNAL, "unknown error");
+    }
+}
+
+wg_status finish_plan(wg::Transforms&& tr, wg_dtype dtype, wg_plan* out) {
+    if (tr.alpha > wg::kMaxAlpha || tr.tile_in > wg::kMaxTile)
+        return fail(WG_ERR_UNSUPPORTED, "alpha' and the input tile must be at most 16");
+    auto* p = new wg_plan_s();
+    p->tr = std::move(tr);
+    p->dtype = static_cast<int>(dtype);
+    const int al = p->tr.alpha, t = p->tr.tile_in, m = p->tr.m;
+    // B^T (alpha x t), G (alpha x 3), A^T (m x alpha), densely packed
+    for (int a = 0; a < al; ++a)
+        for (int u = 0; u < t; ++u) p->itab.bt[a * t + u] = p->tr.Bf[static_cast<size_t>(u * al + a)];
+    for (int a = 0; a < al; ++a)
+        for (int i = 0; i < 3; ++i) p->ktab.g[a * 3 + i] = p->tr.Gf[static_cast<size_t>(a * 3 + i)];
+    for (int o = 0; o < m; ++o)
+        for (int a = 0; a < al; ++a) p->otab.at[o * al + a] = p->tr.Af[static_cast<size_t>(a * m + o)];
+    *out = p;
+    return WG_OK;
+}
+
+wg_status check_create_args(int m, int r, wg_dtype dtype, wg_plan* out) {
+    if (!out) return fail(WG_ERR_ARG, "null output pointer");
+    if (r != 3) return fail(WG_ERR_UNSUPPORTED, "only 3x3 kernels (r = 3) are supported");
+    if (m < 1 || m + r - 1 > wg::kMaxTile) return fail(WG_ERR_UNSUPPORTED, "output tile m out of range");
+    if (dtype != WG_F32 && dtype != WG_F16 && dtype != WG_BF16) return fail(WG_ERR_UNSUPPORTED, "unknown dtype");
+    return WG_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Layout {
+    wg::Geometry g;
+    size_t u_off, v_off, m_off, total;
+};
+
+size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+Layout layout_for(const wg_plan_s* p, int64_t N, int64_t H, int64_t W, int64_t C, int64_t K) {
+    Layout L;
+    L.g = wg::make_geometry(N, H, W, C, K, p->tr.m, p->tr.alpha);
+    const size_t es = static_cast<size_t>(wg::dtype_bytes(p->dtype));
+    const size_t a2 = static_cast<size_t>(p->tr.alpha) * static_cast<size_t>(p->tr.alpha);
+    const size_t ub = a2 * static_cast<size_t>(K) * static_cast<size_t>(L.g.Cp) * es;
+    const size_t vb = a2 * static_cast<size_t>(L.g.T) * static_cast<size_t>(L.g.Cp) * es;
+    const size_t mb = a2 * static_cast<size_t>(L.g.T) * static_cast<size_t>(L.g.Kp) * sizeof(float);
+    L.u_off = 0;
+    L.v_off = align256(ub);
+    L.m_off = L.v_off + align256(vb);
+    L.total = L.m_off + align256(mb);
+    return L;
+}
+
+bool dims_ok(int64_t N, int64_t H, int64_t W, int64_t C, int64_t K) {
+    const int64_t lim = int64_t(1) << 31;
+    return N >= 1 && H >= 1 && W >= 1 && C >= 1 && K >= 1 && N < lim && H < lim && W < lim && C < lim && K < lim;
+}
+
+wg_status check_plan(wg_plan plan) {
+    if (!plan) return fail(WG_ERR_ARG, "null plan");
+    if (!wg::transform_shape_supported(plan->tr.tile_in, plan->tr.alpha))
+        return fail(WG_ERR_UNSUPPORTED, "no compiled transform kernel for input tile " +
+                                            std::to_string(plan->tr.tile_in) + " and alpha' " +
+                                            std::to_string(plan->tr.alpha));
+    return WG_OK;
+}
+
+wg_status check_tensor(const wg_tensor* t, const char* name) {
+    if (!t || !t->data) return fail(WG_ERR_ARG, std::string("null tensor ") + name);
+    if (!aligned16(t->data)) return fail(WG_ERR_ARG, std::string("tensor ") + name + " is not 16-byte aligned");
+    return WG_OK;
+}
+
+hipError_t launch_kt(int dt, const wg::Geometry& g, const wg::KernelTable& t, const void* w, void* U,
+                     hipStream_t s) {
+    switch (dt) {
+        case 0: return wg::launch_kernel_transform_t<0>(g, t, w, U, s);
+        case 1: return wg::launch_kernel_transform_t<1>(g, t, w, U, s);
+        default: return wg::launch_kernel_transform_t<2>(g, t, w, U, s);
+    }
+}
+hipError_t launch_it(int dt, const wg::Geometry& g, const wg::InputTable& t, const void* x, void* V,
+                     hipStream_t s) {
+    switch (dt) {
+        case 0: return wg::launch_input_transform_t<0>(g, t, x, V, s);
+        case 1: return wg::launch_input_transform_t<1>(g, t, x, V, s);
+        default: return wg::launch_input_transform_t<2>(g, t, x, V, s);
+    }
+}
+hipError_t launch_ct(int dt, const wg::Geometry& g, const void* V, const void* U, float* M, hipStream_t s) {
+    switch (dt) {
+        case 0: return wg::launch_contract_t<0>(g, V, U, M, s);
+        case 1: return wg::launch_contract_t<1>(g, V, U, M, s);
+        default: return wg::launch_contract_t<2>(g, V, U, M, s);
+    }
+}
+hipError_t launch_ot(int dt, const wg::Geometry& g, const wg::OutputTable& t, const float* M, void* y,
+                     hipStream_t s) {
+    switch (dt) {
+        case 0: return wg::launch_output_transform_t<0>(g, t, M, y, s);
+        case 1: return wg::launch_output_transform_t<1>(g, t, M, y, s);
+        default: return wg::launch_output_transform_t<2>(g, t, M, y, s);
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+wg_status winograd_plan_create(const wg_poly_set* set, int m, int r, wg_dtype dtype, wg_plan* out) {
+    return guarded([&]() -> wg_status {
+        wg_status s = check_create_args(m, r, dtype, out);
+        if (s != WG_OK) return s;
+        if (!set || set->n_mod <= 0 || !set->mods) return fail(WG_ERR_ARG, "empty modulus set");
+        std::vector<wg::Modulus> mods;
+        for (int i = 0; i < set->n_mod; ++i) {
+            const wg_modulus& md = set->mods[i];
+            wg::Modulus x;
+            if (md.degree == 0) {
+                x.inf = true;
+            } else {
+                if (md.degree < 0 || md.degree > 3) return fail(WG_ERR_UNSUPPORTED, "modulus degree must be 1..3");
+                std::vector<wg::Rat> c;
+                for (int k = 0; k <= md.degree; ++k) {
+                    if (md.coef[k].den == 0) return fail(WG_ERR_ARG, "zero denominator in a modulus");
+                    c.emplace_back(md.coef[k].num, md.coef[k].den);
+                }
+                x.p = wg::Poly(c);
+                if (x.p.deg() != md.degree) return fail(WG_ERR_ARG, "leading coefficient of a modulus is zero");
+            }
+            mods.push_back(x);
+        }
+        std::vector<wg::Rat> inner;
+        bool inner_inf = true;
+        if (set->n_inner > 0) {
+            if (!set->inner_pts) return fail(WG_ERR_ARG, "null inner points");
+            for (int i = 0; i < set->n_inner; ++i) {
+                if (set->inner_pts[i].den == 0) return fail(WG_ERR_ARG, "zero denominator in an inner point");
+                inner.emplace_back(set->inner_pts[i].num, set->inner_pts[i].den);
+            }
+            inner_inf = set->inner_inf != 0;
+        } else {
+            inner = {wg::Rat(0), wg::Rat(-1)};
+        }
+        return finish_plan(wg::build_transforms(mods, inner, inner_inf, m, r), dtype, out);
+    });
+}
+
+wg_status winograd_plan_create_str(const char* moduli, const char* inner, int m, int r, wg_dtype dtype,
+                                   wg_plan* out) {
+    return guarded([&]() -> wg_status {
+        wg_status s = check_create_args(m, r, dtype, out);
+        if (s != WG_OK) return s;
+        if (!moduli) return fail(WG_ERR_ARG, "null modulus string");
+        const std::vector<wg::Modulus> mods = wg::parse_moduli(moduli);
+        std::vector<wg::Rat> pts;
+        bool inf = true;
+        if (inner && inner[0] != '\0') wg::parse_points(inner, &pts, &inf);
+        else pts = {wg::Rat(0), wg::Rat(-1)};
+        return finish_plan(wg::build_transforms(mods, pts, inf, m, r), dtype, out);
+    });
+}
+
+void winograd_plan_destroy(wg_plan plan) { delete plan; }
+
+int winograd_plan_alpha(wg_plan plan) { return plan ? plan->tr.alpha : 0; }
+
+wg_status winograd_plan_info(wg_plan plan, int* m, int* r, int* alpha, int* tile_in, int* dtype) {
+    if (!plan) return fail(WG_ERR_ARG, "null plan");
+    if (m) *m = plan->tr.m;
+    if (r) *r = plan->tr.r;
+    if (alpha) *alpha = plan->tr.alpha;
+    if (tile_in) *tile_in = plan->tr.tile_in;
+    if (dtype) *dtype = plan->dtype;
+    return WG_OK;
+}
+
+wg_status winograd_plan_matrix(wg_plan plan, char which, wg_rational* out, size_t cap) {
+    if (!plan || !out) return fail(WG_ERR_ARG, "null argument");
+    const std::vector<wg::Rat>* src = which == 'G' ? &plan->tr.G : which == 'A' ? &plan->tr.A
+                                    : which == 'B' ? &plan->tr.B : nullptr;
+    if (!src) return fail(WG_ERR_ARG, "matrix must be 'G', 'A' or 'B'");
+    if (cap < src->size()) return fail(WG_ERR_ARG, "output capacity too small");
+    for (size_t i = 0; i < src->size(); ++i) out[i] = wg_rational{(*src)[i].num(), (*src)[i].den()};
+    return WG_OK;
+}
+
+wg_status winograd_plan_matrix_f32(wg_plan plan, char which, float* out, size_t cap) {
+    if (!plan || !out) return fail(WG_ERR_ARG, "null argument");
+    const std::vector<float>* src = which == 'G' ? &plan->tr.Gf : which == 'A' ? &plan->tr.Af
+                                  : which == 'B' ? &plan->tr.Bf : nullptr;
+    if (!src) return fail(WG_ERR_ARG, "matrix must be 'G', 'A' or 'B'");
+    if (cap < src->size()) return fail(WG_ERR_ARG, "output capacity too small");
+    std::memcpy(out, src->data(), src->size() * sizeof(float));
+    return WG_OK;
+}
+
+wg_status winograd_plan_ratio(wg_plan plan, int64_t* num, int64_t* den) {
+    if (!plan || !num || !den) return fail(WG_ERR_ARG, "null argument");
+    return guarded([&]() -> wg_status {
+        const wg::Rat q = wg::Rat(int64_t(plan->tr.alpha) * plan->tr.alpha, int64_t(plan->tr.m) * plan->tr.m);
+        *num = q.num();
+        *den = q.den();
+        return WG_OK;
+    });
+}
+
+wg_status winograd_workspace_bytes(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C, int64_t K,
+                                   size_t* bytes) {
+    if (!plan || !bytes) return fail(WG_ERR_ARG, "null argument");
+    if (!dims_ok(N, H, W, C, K)) return fail(WG_ERR_ARG, "layer sizes must be in [1, 2^31)");
+    *bytes = layout_for(plan, N, H, W, C, K).total;
+    return WG_OK;
+}
+
+wg_status winograd_plan_set_workspace(wg_plan plan, void* dev_ptr, size_t bytes) {
+    if (!plan) return fail(WG_ERR_ARG, "null plan");
+    if (dev_ptr && (reinterpret_cast<uintptr_t>(dev_ptr) & 255u) != 0)
+        return fail(WG_ERR_ARG, "workspace must be 256-byte aligned");
+    plan->ws = dev_ptr;
+    plan->ws_bytes = dev_ptr ? bytes : 0;
+    return WG_OK;
+}
+
+wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
+                          hipStream_t stream) {
+    wg_status s = check_plan(plan);
+    if (s != WG_OK) return s;
+    if ((s = check_tensor(x, "x")) != WG_OK || (s = check_tensor(w, "w")) != WG_OK ||
+        (s = check_tensor(y, "y")) != WG_OK)
+        return s;
+    if (w->h != 3 || w->w != 3 || w->c != x->c)
+        return fail(WG_ERR_ARG, "w must be [K][3][3][C] with the input's C");
+    if (y->n != x->n || y->h != x->h || y->w != x->w || y->c != w->n)
+        return fail(WG_ERR_ARG, "y must be [N][H][W][K]");
+    if (!dims_ok(x->n, x->h, x->w, x->c, w->n)) return fail(WG_ERR_ARG, "layer sizes must be in [1, 2^31)");
+    const Layout L = layout_for(plan, x->n, x->h, x->w, x->c, w->n);
+    if (!plan->ws) return fail(WG_ERR_WORKSPACE, "no workspace bound to the plan");
+    if (plan->ws_bytes < L.total)
+        return fail(WG_ERR_WORKSPACE, "workspace too small: need " + std::to_string(L.total) + " bytes");
+    auto* base = static_cast<unsigned char*>(plan->ws);
+    void* U = base + L.u_off;
+    void* V = base + L.v_off;
+    auto* M = reinterpret_cast<float*>(base + L.m_off);
+    const int dt = plan->dtype;
+    if ((s = from_hip(launch_kt(dt, L.g, plan->ktab, w->data, U, stream), "kernel transform")) != WG_OK) return s;
+    if ((s = from_hip(launch_it(dt, L.g, plan->itab, x->data, V, stream), "input transform")) != WG_OK) return s;
+    if ((s = from_hip(launch_ct(dt, L.g, V, U, M, stream), "contraction")) != WG_OK) return s;
+    return from_hip(launch_ot(dt, L.g, plan->otab, M, y->data, stream), "output transform");
+}
+
+wg_status winograd_kernel_transform(wg_plan plan, const wg_tensor* w, void* U, hipStream_t stream) {
+    wg_status s = check_plan(plan);
+    if (s != WG_OK) return s;
+    if ((s = check_tensor(w, "w")) != WG_OK) return s;
+    if (!U || !aligned16(U)) return fail(WG_ERR_ARG, "U must be a 16-byte aligned device pointer");
+    if (w->h != 3 || w->w != 3) return fail(WG_ERR_ARG, "w must be [K][3][3][C]");
+    if (!dims_ok(1, 1, 1, w->c, w->n)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
+    const wg::Geometry g = wg::make_geometry(1, 1, 1, w->c, w->n, plan->tr.m, plan->tr.alpha);
+    return from_hip(launch_kt(plan->dtype, g, plan->ktab, w->data, U, stream), "kernel transform");
+}
+
+wg_status winograd_input_transform(wg_plan plan, const wg_tensor* x, void* V, hipStream_t stream) {
+    wg_status s = check_plan(plan);
+    if (s != WG_OK) return s;
+    if ((s = check_tensor(x, "x")) != WG_OK) return s;
+    if (!V || !aligned16(V)) return fail(WG_ERR_ARG, "V must be a 16-byte aligned device pointer");
+    if (!dims_ok(x->n, x->h, x->w, x->c, 1)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
+    const wg::Geometry g = wg::make_geometry(x->n, x->h, x->w, x->c, 1, plan->tr.m, plan->tr.alpha);
+    return from_hip(launch_it(plan->dtype, g, plan->itab, x->data, V, stream), "input transform");
+}
+
+wg_status winograd_contract(wg_plan plan, const void* V, const void* U, float* M, int64_t T, int64_t C,
+                            int64_t K, hipStream_t stream) {
+    wg_status s = check_plan(plan);
+    if (s != WG_OK) return s;
+    if (!V || !U || !M || !aligned16(V) || !aligned16(U) || !aligned16(M))
+        return fail(WG_ERR_ARG, "V, U and M must be 16-byte aligned device pointers");
+    if (!dims_ok(T, 1, 1, C, K)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
+    wg::Geometry g = wg::make_geometry(1, 1, 1, C, K, plan->tr.m, plan->tr.alpha);
+    g.T = T;
+    return from_hip(launch_ct(plan->dtype, g, V, U, M, stream), "contraction");
+}
+
+wg_status winograd_output_transform(wg_plan plan, const float* M, wg_tensor* y, hipStream_t stream) {
+    wg_status s = check_plan(plan);
+    if (s != WG_OK) return s;
+    if ((s = check_tensor(y, "y")) != WG_OK) return s;
+    if (!M || !aligned16(M)) return fail(WG_ERR_ARG, "M must be a 16-byte aligned device pointer");
+    if (!dims_ok(y->n, y->h, y->w, 1, y->c)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
+    const wg::Geometry g = wg::make_geometry(y->n, y->h, y->w, 1, y->c, plan->tr.m, plan->tr.alpha);
+    return from_hip(launch_ot(plan->dtype, g, plan->otab, M, y->data, stream), "output transform");
+}
+
+const char* winograd_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,49 @@
+// Device-side storage types and conversions (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace wg {
+
+// bf16 kept as its 16 raw bits; arithmetic is always done in fp32.
+struct bf16_t { uint16_t bits; };
+
+template <typename T> struct Storage;
+
+template <> struct Storage<float> {
+    static __device__ __forceinline__ float to_f32(float v) { return v; }
+    static __device__ __forceinline__ float from_f32(float f) { return f; }
+};
+
+template <> struct Storage<_Float16> {
+    static __device__ __forceinline__ float to_f32(_Float16 v) { return static_cast<float>(v); }
+    // IEEE conversion, round to nearest even (the default rounding mode)
+    static __device__ __forceinline__ _Float16 from_f32(float f) { return static_cast<_Float16>(f); }
+};
+
+template <> struct Storage<bf16_t> {
+    static __device__ __forceinline__ float to_f32(bf16_t v) {
+        return __uint_as_float(static_cast<uint32_t>(v.bits) << 16);
+    }
+    // Round to nearest even on the fp32 encoding; NaN stays a quiet NaN.
+    static __device__ __forceinline__ bf16_t from_f32(float f) {
+        uint32_t u = __float_as_uint(f);
+        bf16_t r;
+        if ((u & 0x7fffffffu) > 0x7f800000u) {
+            r.bits = static_cast<uint16_t>((u >> 16) | 0x40u);
+        } else {
+            u += 0x7fffu + ((u >> 16) & 1u);
+            r.bits = static_cast<uint16_t>(u >> 16);
+        }
+        return r;
+    }
+};
+
+template <int D> struct DTypeOf;
+template <> struct DTypeOf<0> { using type = float; };
+template <> struct DTypeOf<1> { using type = _Float16; };
+template <> struct DTypeOf<2> { using type = bf16_t; };
+
+}  // namespace wg

@@ -1,0 +1,248 @@
+// Winograd transforms of eq. (2) (Barabasz & Gregg, arXiv 1905.05233) for
+// gfx950: the kernel transform U = G g G^T, the input transform V = B^T d B
+// and the output transform Y = A^T M A fused with the NHWC store.
+//
+// All three are memory-bound.  Each thread owns one (tile, channel) or
+// (kernel, channel) pair, so a wavefront's loads and stores sweep 64
+// consecutive channels of NHWC / channel-last buffers (coalesced).  The
+// transform matrices arrive by value in the kernel-argument segment (they are
+// uniform across the grid and live in scalar registers); the small matrices
+// are applied as two separable 1D passes in fp32 registers with ascending-index
+// fused multiply-adds, and results are rounded to the storage dtype once, at
+// the store.
+//
+// This file is compiled once per storage dtype (WG_DTYPE = 0 fp32, 1 fp16,
+// 2 bf16); each (input tile, alpha') shape is a template instance so that the
+// register arrays have compile-time sizes.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+#ifndef WG_DTYPE
+#error "compile with -DWG_DTYPE=0|1|2"
+#endif
+
+namespace wg {
+
+namespace {
+
+constexpr int kBlock = 256;
+
+// ----------------------------------------------------------------- kernel
+// U[xi = a*alpha + b][k][c] = sum_j (sum_i G[a][i] g[i][j]) G[b][j]
+template <typename Elem, int ALPHA>
+__global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, const Elem* __restrict__ w,
+                                                           Elem* __restrict__ U, int64_t K, int64_t C,
+                                                           int64_t Cp) {
+    using S = Storage<Elem>;
+    const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (gid >= K * Cp) return;
+    const int64_t c = gid % Cp;
+    const int64_t k = gid / Cp;
+    const int64_t plane = K * Cp;
+    Elem* out = U + k * Cp + c;
+    if (c >= C) {
+#pragma unroll
+        for (int x = 0; x < ALPHA * ALPHA; ++x) out[x * plane] = S::from_f32(0.0f);
+        return;
+    }
+    float g[3][3];
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+#pragma unroll
+        for (int j = 0; j < 3; ++j) g[i][j] = S::to_f32(w[((k * 3 + i) * 3 + j) * C + c]);
+    float Gg[ALPHA][3];
+#pragma unroll
+    for (int a = 0; a < ALPHA; ++a)
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 3; ++i) acc = __builtin_fmaf(tab.g[a * 3 + i], g[i][j], acc);
+            Gg[a][j] = acc;
+        }
+#pragma unroll
+    for (int a = 0; a < ALPHA; ++a)
+#pragma unroll
+        for (int b = 0; b < ALPHA; ++b) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(Gg[a][j], tab.g[b * 3 + j], acc);
+            out[(a * ALPHA + b) * plane] = S::from_f32(acc);
+        }
+}
+
+// ------------------------------------------------------------------ input
+// V[xi = a*alpha + b][tile][c] = sum_v (sum_u B^T[a][u] d[u][v]) B^T[b][v],
+// d = the (m+2)^2 window whose top-left pixel is (ty*m - 1, tx*m - 1).
+template <typename Elem, int TT, int ALPHA>
+__global__ __launch_bounds__(kBlock) void input_transform(InputTable tab, const Elem* __restrict__ x,
+                                                          Elem* __restrict__ V, Geometry geo) {
+    using S = Storage<Elem>;
+    const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (gid >= geo.T * geo.Cp) return;
+    const int64_t c = gid % geo.Cp;
+    const int64_t tile = gid / geo.Cp;
+    const int64_t plane = geo.T * geo.Cp;
+    Elem* out = V + tile * geo.Cp + c;
+    if (c >= geo.C) {
+#pragma unroll
+        for (int xi = 0; xi < ALPHA * ALPHA; ++xi) out[xi * plane] = S::from_f32(0.0f);
+        return;
+    }
+    const int64_t tx = tile % geo.tw;
+    const int64_t ty = (tile / geo.tw) % geo.th;
+    const int64_t n = tile / (geo.tw * geo.th);
+    const int64_t h0 = ty * geo.m - 1;
+    const int64_t w0 = tx * geo.m - 1;
+    const Elem* xn = x + n * geo.H * geo.W * geo.C + c;
+
+    // pass 1, one input column at a time: W1[a][v] = sum_u B^T[a][u] d[u][v]
+    float W1[ALPHA][TT];
+#pragma unroll
+    for (int v = 0; v < TT; ++v) {
+        const int64_t wc = w0 + v;
+        const bool col_ok = wc >= 0 && wc < geo.W;
+        float col[TT];
+#pragma unroll
+        for (int u = 0; u < TT; ++u) {
+            const int64_t hr = h0 + u;
+            col[u] = (col_ok && hr >= 0 && hr < geo.H) ? S::to_f32(xn[(hr * geo.W + wc) * geo.C]) : 0.0f;
+        }
+#pragma unroll
+        for (int a = 0; a < ALPHA; ++a) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int u = 0; u < TT; ++u) acc = __builtin_fmaf(tab.bt[a * TT + u], col[u], acc);
+            W1[a][v] = acc;
+        }
+    }
+    // pass 2, one output row at a time: V[a][b] = sum_v W1[a][v] B^T[b][v]
+#pragma unroll
+    for (int a = 0; a < ALPHA; ++a)
+#pragma unroll
+        for (int b = 0; b < ALPHA; ++b) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int v = 0; v < TT; ++v) acc = __builtin_fmaf(W1[a][v], tab.bt[b * TT + v], acc);
+            out[(a * ALPHA + b) * plane] = S::from_f32(acc);
+        }
+}
+
+// ----------------------------------------------------------------- output
+// y[n][ty*m+o][tx*m+p][k] = sum_b (sum_a A^T[o][a] M[a][b]) A^T[p][b]
+template <typename Elem, int MM, int ALPHA>
+__global__ __launch_bounds__(kBlock) void output_transform(OutputTable tab, const float* __restrict__ Mx,
+                                                           Elem* __restrict__ y, Geometry geo) {
+    using S = Storage<Elem>;
+    const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (gid >= geo.T * geo.K) return;
+    const int64_t k = gid % geo.K;
+    const int64_t tile = gid / geo.K;
+    const int64_t plane = geo.T * geo.Kp;
+    const float* in = Mx + tile * geo.Kp + k;
+    const int64_t tx = tile % geo.tw;
+    const int64_t ty = (tile / geo.tw) % geo.th;
+    const int64_t n = tile / (geo.tw * geo.th);
+
+    // pass 1, one domain column at a time: Z[o][b] = sum_a A^T[o][a] M[a][b]
+    float Z[MM][ALPHA];
+#pragma unroll
+    for (int b = 0; b < ALPHA; ++b) {
+        float col[ALPHA];
+#pragma unroll
+        for (int a = 0; a < ALPHA; ++a) col[a] = in[(a * ALPHA + b) * plane];
+#pragma unroll
+        for (int o = 0; o < MM; ++o) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int a = 0; a < ALPHA; ++a) acc = __builtin_fmaf(tab.at[o * ALPHA + a], col[a], acc);
+            Z[o][b] = acc;
+        }
+    }
+    // pass 2 and the masked NHWC store
+    Elem* yn = y + n * geo.H * geo.W * geo.K + k;
+#pragma unroll
+    for (int o = 0; o < MM; ++o) {
+        const int64_t hr = ty * MM + o;
+        if (hr >= geo.H) break;
+#pragma unroll
+        for (int p = 0; p < MM; ++p) {
+            const int64_t wc = tx * MM + p;
+            float acc = 0.0f;
+#pragma unroll
+            for (int b = 0; b < ALPHA; ++b) acc = __builtin_fmaf(Z[o][b], tab.at[p * ALPHA + b], acc);
+            if (wc < geo.W) yn[(hr * geo.W + wc) * geo.K] = S::from_f32(acc);
+        }
+    }
+}
+
+inline unsigned blocks_for(int64_t n) { return static_cast<unsigned>((n + kBlock - 1) / kBlock); }
+
+}  // namespace
+
+// ------------------------------------------------------------- launchers
+
+template <int D>
+hipError_t launch_kernel_transform_t(const Geometry& g, const KernelTable& tab, const void* w, void* U,
+                                     hipStream_t stream) {
+    using Elem = typename DTypeOf<D>::type;
+    const auto* wp = static_cast<const Elem*>(w);
+    auto* up = static_cast<Elem*>(U);
+    const unsigned nb = blocks_for(g.K * g.Cp);
+    switch (g.alpha) {
+#define WG_KT_CASE(A)                                                                             \
+    case A:                                                                                       \
+        hipLaunchKernelGGL((kernel_transform<Elem, A>), dim3(nb), dim3(kBlock), 0, stream, tab, wp, up, g.K, \
+                           g.C, g.Cp);                                                            \
+        break;
+        WG_KT_CASE(4) WG_KT_CASE(5) WG_KT_CASE(6) WG_KT_CASE(7) WG_KT_CASE(8) WG_KT_CASE(9)
+        WG_KT_CASE(10) WG_KT_CASE(11) WG_KT_CASE(12) WG_KT_CASE(13) WG_KT_CASE(14) WG_KT_CASE(15)
+        WG_KT_CASE(16)
+#undef WG_KT_CASE
+        default:
+            return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_input_transform_t(const Geometry& g, const InputTable& tab, const void* x, void* V,
+                                    hipStream_t stream) {
+    using Elem = typename DTypeOf<D>::type;
+    const auto* xp = static_cast<const Elem*>(x);
+    auto* vp = static_cast<Elem*>(V);
+    const unsigned nb = blocks_for(g.T * g.Cp);
+#define WG_IT_CASE(TT, A)                                                                               \
+    if (g.t == TT && g.alpha == A) {                                                                    \
+        hipLaunchKernelGGL((input_transform<Elem, TT, A>), dim3(nb), dim3(kBlock), 0, stream, tab, xp, vp, g); \
+        return hipGetLastError();                                                                       \
+    }
+    WG_TRANSFORM_SHAPES(WG_IT_CASE)
+#undef WG_IT_CASE
+    return hipErrorInvalidValue;
+}
+
+template <int D>
+hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, const float* M, void* y,
+                                     hipStream_t stream) {
+    using Elem = typename DTypeOf<D>::type;
+    auto* yp = static_cast<Elem*>(y);
+    const unsigned nb = blocks_for(g.T * g.K);
+#define WG_OT_CASE(TT, A)                                                                                   \
+    if (g.t == TT && g.alpha == A) {                                                                        \
+        hipLaunchKernelGGL((output_transform<Elem, TT - 2, A>), dim3(nb), dim3(kBlock), 0, stream, tab, M, yp, g); \
+        return hipGetLastError();                                                                           \
+    }
+    WG_TRANSFORM_SHAPES(WG_OT_CASE)
+#undef WG_OT_CASE
+    return hipErrorInvalidValue;
+}
+
+template hipError_t launch_kernel_transform_t<WG_DTYPE>(const Geometry&, const KernelTable&, const void*, void*,
+                                                        hipStream_t);
+template hipError_t launch_input_transform_t<WG_DTYPE>(const Geometry&, const InputTable&, const void*, void*,
+                                                       hipStream_t);
+template hipError_t launch_output_transform_t<WG_DTYPE>(const Geometry&, const OutputTable&, const float*, void*,
+                                                        hipStream_t);
+
+}  // namespace wg

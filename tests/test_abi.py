@@ -1,0 +1,168 @@
+"""C-ABI library on the CPU: it loads, exports every symbol the header
+declares, builds plans whose exact matrices and fp32 tables equal the oracle's
+bit for bit, and rejects invalid input with the documented status codes.
+No kernel is launched here."""
+import ctypes
+import os
+import re
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from conftest import ROOT, load_golden
+from oracle import conv as OC
+from oracle import fp as OF
+from oracle import plan as OP
+from paper_1905_05233_amd import _native as N
+from paper_1905_05233_amd import workloads as WL
+from paper_1905_05233_amd.winograd import Plan
+
+HEADER = os.path.join(ROOT, "include", "winograd_crt.h")
+
+PLAN_SETS = [
+    (WL.F2_LINEAR, 2, "0,-1,inf"), (WL.F4_LINEAR, 4, "0,-1,inf"), (WL.F4_A2P1, 4, "0,-1,inf"),
+    (WL.F6_LINEAR, 6, "0,-1,inf"), (WL.F6_TWO_QUAD, 6, "0,-1,inf"), (WL.F6_ONE_A2P1, 6, "0,-1,inf"),
+    ("0,a^2+1,inf", 2, "0,1,inf"), ("0,a^2+a+1,inf", 2, "0,1,inf"), ("0,a^2-2,inf", 2, "0,-1,inf"),
+    ("a^2+1,a^2+a+1", 2, "0,-1,inf"), ("a^2+1,a^2+a+1,a^2-a+1", 4, "0,-1,inf"),
+    ("0,a^3+2", 2, "0,-1,1,-2,inf"), ("0,1,-1,2,-2,inf", 4, "0,-1,inf"),
+    ("0,-1,1,-1/2,2,1/2,-2,a^2+1,inf", 8, "0,-1,inf"),
+    ("0,-1,1,-1/2,2,1/2,-2,-1/4,4,a^2+1,inf", 10, "0,-1,inf"),
+]
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\**\s*(winograd_\w+)\s*\(", text, re.M)))
+
+
+def test_library_loads_and_exports_every_symbol():
+    lib = N.lib()
+    names = header_functions()
+    assert len(names) >= 15
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+@pytest.mark.parametrize("spec,m,inner", PLAN_SETS)
+def test_plan_exact_parity_with_oracle(spec, m, inner):
+    ref = OP.build_plan(spec, n_o=m, inner=inner)
+    p = Plan(spec, m=m, dtype="f32", inner=inner)
+    assert p.alpha == ref.alpha and p.tile_in == ref.tile_in
+    assert p.matrix("G") == ref.G
+    assert p.matrix("A") == ref.A
+    assert p.matrix("B") == ref.B
+    assert p.ratio == ref.ratio
+    for which, mat in (("G", ref.G), ("A", ref.A), ("B", ref.B)):
+        ours = np.array(p.matrix_f32(which), dtype=np.float32)
+        want = np.array([[OF.fraction_to_f32(v) for v in row] for row in mat], dtype=np.float32)
+        assert np.array_equal(ours.view(np.uint32), want.view(np.uint32)), which
+
+
+def test_struct_entry_matches_string_entry():
+    p1 = Plan(WL.F6_TWO_QUAD, m=6, dtype="bf16")
+    mods = [[0, 1], [1, 1], [-1, 1], [1, 0, 1], [-2, 0, 1], None]
+    p2 = Plan.from_moduli(mods, m=6, dtype="bf16", inner_points=[0, -1], inner_inf=True)
+    for w in "GAB":
+        assert p1.matrix(w) == p2.matrix(w)
+
+
+def test_non_monic_moduli_are_normalised():
+    p1 = Plan("0,1,-1,a^2+1,inf", m=4)
+    p2 = Plan.from_moduli([[0, 2], [-3, 3], [1, 1], [2, 0, 2], None], m=4)
+    for w in "GAB":
+        assert p1.matrix(w) == p2.matrix(w)
+
+
+def test_worked_example_through_the_library():
+    """Section 2.2's printed G^W and (at b=0, c=1) B^W, via the C ABI."""
+    from conftest import frac_matrix
+    gold = load_golden("worked_example_sec2_2.json")
+    for b, c in [(0, 1), (1, 1), (0, -2)]:
+        p = Plan.from_moduli([[0, 1], [c, b, 1], None], m=2, inner_points=[0, 1], inner_inf=True)
+        env = {"b": Fraction(b), "c": Fraction(c)}
+        assert p.matrix("G") == frac_matrix(gold["general"]["G_W"], env)
+    p = Plan("0,a^2+1,inf", m=2, inner="0,1,inf")
+    assert p.matrix("B") == frac_matrix(gold["b0c1"]["B_W"], {"b": Fraction(0), "c": Fraction(1)})
+
+
+@pytest.mark.parametrize("spec,m,inner,code", [
+    ("0,1,inf", 4, "", 2),                        # degree sum
+    ("0,1,-1,a^2+1,a^2+1,inf", 6, "", 3),         # not coprime
+    ("0,0,1,-1,1/2,inf", 4, "", 3),               # repeated point
+    ("0,1,-1,a^2-1,inf", 4, "", 4),               # reducible
+    ("0,1,-1,a^2-4a+4,inf", 4, "", 4),            # reducible (double root)
+    ("0,1,x,inf", 2, "", 1),                      # parse error
+    ("0,1,-1,1/0,inf", 4, "", 1),                 # zero denominator
+    ("0,a^2+1,inf", 2, "0,inf", 1),               # too few inner points
+    ("0,a^2+1,inf", 2, "0,0,inf", 1),             # repeated inner point
+    ("0,1,inf,-1,inf", 2, "", 1),                 # infinity twice
+    ("0,1,-1,99999999999999999999,inf", 2, "", 6),  # out of int64
+])
+def test_invalid_plans_rejected(spec, m, inner, code):
+    with pytest.raises(N.WinogradError) as ei:
+        Plan(spec, m=m, inner=inner)
+    assert ei.value.status == code
+    assert str(ei.value)
+
+
+def test_unsupported_shapes_rejected():
+    with pytest.raises(N.WinogradError) as ei:
+        Plan("0,1,-1,inf", m=2, r=5)
+    assert ei.value.status == 5
+    pts = ",".join(str(i) for i in range(-8, 8))      # m = 15 -> tile 17 > 16
+    with pytest.raises(N.WinogradError) as ei:
+        Plan(pts + ",inf", m=15)
+    assert ei.value.status == 5
+    with pytest.raises(ValueError):
+        Plan("0,1,-1,inf", m=2, dtype="f64")
+
+
+def test_exact_overflow_is_reported():
+    """Points whose Lagrange denominators leave int64 must raise, not wrap."""
+    big = [str(Fraction(1, 3 ** k)) for k in range(1, 11)]
+    with pytest.raises(N.WinogradError) as ei:
+        Plan(",".join(["0"] + big) + ",inf", m=10)
+    assert ei.value.status in (6,)
+
+
+def test_workspace_bytes_and_errors():
+    p = Plan(WL.F4_LINEAR, m=4, dtype="f32")
+    Nn, H, W, C, K = 8, 56, 56, 128, 128
+    T = Nn * 14 * 14
+    need = p.workspace_bytes(Nn, H, W, C, K)
+    a2 = 36
+    assert need >= a2 * (K * C * 4 + T * C * 4 + T * K * 4)
+    assert need <= a2 * (K * C * 4 + T * C * 4 + T * K * 4) + 3 * 256
+    with pytest.raises(N.WinogradError) as ei:
+        p.workspace_bytes(0, H, W, C, K)
+    assert ei.value.status == 1
+    lib = N.lib()
+    fake = ctypes.c_void_p(1 << 20)   # aligned, never dereferenced: the call fails before any launch
+    x = N.WgTensor(fake, Nn, H, W, C)
+    w = N.WgTensor(fake, K, 3, 3, C)
+    y = N.WgTensor(fake, Nn, H, W, K)
+    st = lib.winograd_conv2d(p._h, ctypes.byref(x), ctypes.byref(w), ctypes.byref(y), None)
+    assert st == 7 and b"workspace" in lib.winograd_last_error()
+    bad = N.WgTensor(ctypes.c_void_p((1 << 20) + 4), Nn, H, W, C)
+    assert lib.winograd_conv2d(p._h, ctypes.byref(bad), ctypes.byref(w), ctypes.byref(y), None) == 1
+    wrong = N.WgTensor(fake, K, 3, 3, C + 1)
+    assert lib.winograd_conv2d(p._h, ctypes.byref(x), ctypes.byref(wrong), ctypes.byref(y), None) == 1
+    assert lib.winograd_conv2d(None, ctypes.byref(x), ctypes.byref(w), ctypes.byref(y), None) == 1
+    assert lib.winograd_plan_set_workspace(p._h, ctypes.c_void_p((1 << 20) + 16), 4096) == 1
+
+
+def test_unsupported_kernel_shape_reported_at_launch():
+    """A valid plan whose (tile, alpha') has no compiled kernel fails cleanly."""
+    p = Plan("0,1,-1,1/2,inf", m=3)      # tile 5: odd m has no transform kernels
+    lib = N.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    x = N.WgTensor(fake, 1, 8, 8, 4)
+    assert lib.winograd_input_transform(p._h, ctypes.byref(x), fake, None) == 5
+
+
+def test_geometry_helpers():
+    p = Plan(WL.F6_LINEAR, m=6, dtype="bf16")
+    g = p.geometry(16, 28, 28, 256, 256)
+    assert g["T"] == 16 * 5 * 5 and g["Cp"] == 256
+    assert OC.tile_counts(28, 28, 6) == (5, 5)

@@ -1,0 +1,140 @@
+"""Per-kernel parity on the GPU through the C ABI stage entry points.
+
+Bit-exact where every rounding is exact (dyadic transforms, small-integer
+data): this pins tile indexing, the Winograd-domain index xi = i*alpha' + j,
+the channel padding and the GEMM lane layouts.  Elsewhere each stage is held
+to the rounding bound of its own arithmetic against the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import TORCH, to_dev, to_np
+from oracle import conv as OC
+from oracle import fp as OF
+from oracle import plan as OP
+from paper_1905_05233_amd import workloads as WL
+
+pytestmark = pytest.mark.gpu
+
+DYADIC = [(WL.F2_LINEAR, 2), (WL.F4_A2P1, 4), ("0,a^2+1,inf", 2)]
+GENERAL = [(WL.F4_LINEAR, 4), (WL.F6_LINEAR, 6), (WL.F6_TWO_QUAD, 6), (WL.F6_ONE_A2P1, 6)]
+DTYPES = ["f32", "f16", "bf16"]
+
+
+def _plan(spec, m, dtype, inner="0,-1,inf"):
+    from paper_1905_05233_amd.winograd import Plan
+    print(f"[stage] plan {spec} m={m} dtype={dtype}", flush=True)
+    return Plan(spec, m=m, dtype=dtype, inner=inner), OP.build_plan(spec, n_o=m, inner=inner)
+
+
+@pytest.mark.parametrize("spec,m", DYADIC)
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("shape", [(2, 9, 7, 5), (1, 1, 1, 3), (3, 16, 13, 40)])
+def test_input_transform_bit_exact(spec, m, dtype, shape):
+    p, op = _plan(spec, m, dtype)
+    N, H, W, C = shape
+    dist = "ternary" if dtype == "bf16" else "int2"
+    x, _ = WL.draw_inputs(N, H, W, C, 1, dist, seed=H * 31 + W)
+    V = to_np(p.input_transform(to_dev(x, dtype)))
+    torch.cuda.synchronize()
+    ref = OC.input_transform_emulated(x, op, dtype)
+    al = op.alpha
+    ref = ref.reshape(al * al, -1, C)
+    assert V.shape[:2] == ref.shape[:2]
+    assert np.array_equal(V[:, :, :C], ref)
+    assert np.all(V[:, :, C:] == 0)
+
+
+@pytest.mark.parametrize("spec,m", GENERAL)
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_input_transform_within_bound(spec, m, dtype):
+    p, op = _plan(spec, m, dtype)
+    N, H, W, C = 2, 2 * m + 3, 3 * m - 1, 24
+    x, _ = WL.draw_inputs(N, H, W, C, 1, "uniform", seed=5)
+    x = OF.to_dtype(x, dtype)
+    V = to_np(p.input_transform(to_dev(x, dtype)))[:, :, :C]
+    ref = OC.input_transform_emulated(x, op, dtype).reshape(op.alpha ** 2, -1, C)
+    B = np.abs(np.array([[float(v) for v in r] for r in op.B]))
+    d = np.abs(OC._windows(x.astype(np.float64), m))
+    Vabs = np.einsum("ua,nxyuvc,vb->abnxyc", B, d, B).reshape(op.alpha ** 2, -1, C)
+    u32, ud = 2.0 ** -24, OF.UNIT_ROUNDOFF[dtype]
+    # each side: fp32 table rounding and two t-term passes, then one dtype rounding
+    tol = 2 * ((2 * op.tile_in + 2) * u32 * 1.1 * Vabs + ud * np.maximum(np.abs(ref), np.abs(V)))
+    assert np.all(np.abs(V - ref) <= tol)
+
+
+@pytest.mark.parametrize("spec,m", DYADIC + GENERAL)
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_kernel_transform(spec, m, dtype):
+    p, op = _plan(spec, m, dtype)
+    K, C = 7, 13
+    dist = "ternary" if dtype == "bf16" else "int2"
+    _, w = WL.draw_inputs(1, 1, 1, C, K, dist, seed=K + C)
+    U = to_np(p.kernel_transform(to_dev(w, dtype)))
+    ref = OC.kernel_transform_emulated(w, op, dtype).reshape(op.alpha ** 2, K, C)
+    assert np.all(U[:, :, C:] == 0)
+    if (spec, m) in DYADIC:
+        assert np.array_equal(U[:, :, :C], ref)
+    else:
+        G = np.abs(np.array([[float(v) for v in r] for r in op.G]))
+        Uabs = np.einsum("ai,kijc,bj->abkc", G, np.abs(w.astype(np.float64)), G).reshape(op.alpha ** 2, K, C)
+        u32, ud = 2.0 ** -24, OF.UNIT_ROUNDOFF[dtype]
+        tol = 2 * (8 * u32 * 1.1 * Uabs + ud * np.maximum(np.abs(ref), np.abs(U[:, :, :C])))
+        assert np.all(np.abs(U[:, :, :C] - ref) <= tol)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("T,C,K", [(1, 1, 1), (37, 8, 5), (129, 40, 130), (300, 264, 96), (1568, 128, 128)])
+def test_contract_bit_exact_on_integers(dtype, T, C, K):
+    p, _ = _plan(WL.F4_A2P1, 4, dtype)
+    a2 = p.alpha ** 2
+    Cp = -(-C // 8) * 8
+    rng = np.random.Generator(np.random.PCG64(T + C + K))
+    V = np.zeros((a2, T, Cp), np.float32)
+    U = np.zeros((a2, K, Cp), np.float32)
+    V[:, :, :C] = rng.integers(-3, 4, size=(a2, T, C))
+    U[:, :, :C] = rng.integers(-3, 4, size=(a2, K, C))
+    M = to_np(p.contract(to_dev(V, dtype), to_dev(U, dtype), C))
+    ref = np.einsum("xtc,xkc->xtk", V.astype(np.float64), U.astype(np.float64))
+    assert np.array_equal(M[:, :, :K].astype(np.float64), ref)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_contract_random_within_bound(dtype):
+    p, _ = _plan(WL.F6_TWO_QUAD, 6, dtype)
+    a2, T, C, K = p.alpha ** 2, 200, 256, 72
+    rng = np.random.Generator(np.random.PCG64(3))
+    V = OF.to_dtype(rng.standard_normal((a2, T, C)).astype(np.float32), dtype)
+    U = OF.to_dtype(rng.standard_normal((a2, K, C)).astype(np.float32), dtype)
+    M = to_np(p.contract(to_dev(V, dtype), to_dev(U, dtype), C))[:, :, :K]
+    ref = np.einsum("xtc,xkc->xtk", V.astype(np.float64), U.astype(np.float64))
+    mag = np.einsum("xtc,xkc->xtk", np.abs(V).astype(np.float64), np.abs(U).astype(np.float64))
+    u32 = 2.0 ** -24
+    # fp32 products (exact for fp16/bf16) and a C-term fp32 sum
+    assert np.all(np.abs(M - ref) <= (C + 1) * u32 * 1.1 * mag)
+
+
+@pytest.mark.parametrize("spec,m", DYADIC + GENERAL)
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_output_transform(spec, m, dtype):
+    p, op = _plan(spec, m, dtype)
+    N, H, W, K = 2, 2 * m + 1, m + 3, 11
+    g = p.geometry(N, H, W, 1, K)
+    al = op.alpha
+    rng = np.random.Generator(np.random.PCG64(7))
+    Mx = np.zeros((al * al, g["T"], g["Kp"]), np.float32)
+    Mx[:, :, :K] = rng.integers(-3, 4, size=(al * al, g["T"], K))
+    y = to_np(p.output_transform(torch.from_numpy(Mx).cuda(), N, H, W, K))
+    th, tw = g["th"], g["tw"]
+    Mo = Mx[:, :, :K].reshape(al, al, N, th, tw, K)
+    ref = OC.output_transform_emulated(Mo, op, dtype, H, W)
+    if (spec, m) in DYADIC and dtype != "bf16":
+        assert np.array_equal(y, ref)
+    else:
+        A = np.abs(np.array([[float(v) for v in r] for r in op.A]))
+        Yabs = np.einsum("ao,abnxyk,bp->nxoypk", A, np.abs(Mo.astype(np.float64)), A)
+        Yabs = Yabs.reshape(N, th * m, tw * m, K)[:, :H, :W, :]
+        u32, ud = 2.0 ** -24, OF.UNIT_ROUNDOFF[dtype]
+        tol = 2 * ((2 * al + 2) * u32 * 1.1 * Yabs + ud * np.maximum(np.abs(ref), np.abs(y)))
+        assert np.all(np.abs(y - ref) <= tol)
