@@ -87,8 +87,9 @@ def main(argv=None):
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="CPU oracle time budget (0 disables the cpu_baseline leg)")
     ap.add_argument("--graph", action="store_true", help="replay each step from a captured HIP graph")
-    ap.add_argument("--profile-kernel", default=None, choices=KERNEL_NAMES,
-                    help="only launch this kernel, --steps times (for counter collection)")
+    ap.add_argument("--profile-kernel", default=None, choices=KERNEL_NAMES + ("copy",),
+                    help="only launch this kernel, --steps times (for counter collection); 'copy' "
+                         "launches a plain 256 MiB device copy to calibrate the byte counters")
     a = ap.parse_args(argv)
 
     if a.gpus != 1:
@@ -141,6 +142,16 @@ def main(argv=None):
                                                                   ctypes.byref(yt), sh),
     }
 
+    if a.profile_kernel == "copy":
+        src = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(a.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"profiled": "copy", "bytes_read_per_launch": src.numel() * 4,
+                          "bytes_written_per_launch": dst.numel() * 4, "launches": a.steps}))
+        return 0
     if a.profile_kernel:
         for name in KERNEL_NAMES:       # produce valid inputs for the profiled kernel
             NAT.check(stages[name]())
@@ -176,19 +187,24 @@ def main(argv=None):
     value = wl.direct_flops / (ms_per_step * 1e-3) / 1e12
 
     # ------------------------------------------- per-kernel event timing
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(KERNEL_NAMES) + 1)] for _ in range(a.steps)]
-    for _ in range(3):
-        for name in KERNEL_NAMES:
-            NAT.check(stages[name]())
+    # Each kernel is launched --steps times back to back on the bench stream
+    # between two HIP events (its inputs are valid: every stage ran first).
+    for name in KERNEL_NAMES:
+        NAT.check(stages[name]())
     torch.cuda.synchronize()
-    for it in range(a.steps):
-        ev[it][0].record(stream)
-        for k, name in enumerate(KERNEL_NAMES):
-            NAT.check(stages[name]())
-            ev[it][k + 1].record(stream)
-    torch.cuda.synchronize()
-    kernel_us = {name: 1e3 * sum(ev[it][k].elapsed_time(ev[it][k + 1]) for it in range(a.steps)) / a.steps
-                 for k, name in enumerate(KERNEL_NAMES)}
+    kernel_us = {}
+    for name in KERNEL_NAMES:
+        fn = stages[name]
+        for _ in range(3):
+            fn()
+        k0 = torch.cuda.Event(enable_timing=True)
+        k1 = torch.cuda.Event(enable_timing=True)
+        k0.record(stream)
+        for _ in range(a.steps):
+            fn()
+        k1.record(stream)
+        torch.cuda.synchronize()
+        kernel_us[name] = 1e3 * k0.elapsed_time(k1) / a.steps
 
     wtag = a.workload + (f"p{a.plan}" if a.plan else "")
     kernels = {}
