@@ -45,10 +45,19 @@ def _run(cmd):
     return out
 
 
-def compile_unit(unit):
+def _newest_header():
+    hdrs = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hpp")]
+    hdrs.append(os.path.join(INCLUDE, "winograd_crt.h"))
+    return max(os.path.getmtime(h) for h in hdrs)
+
+
+def compile_unit(unit, incremental=False):
     src, extra, obj = unit
     path = os.path.join(CSRC, src)
     out = os.path.join(BUILD, obj)
+    if incremental and os.path.exists(out):
+        if os.path.getmtime(out) > max(os.path.getmtime(path), _newest_header()):
+            return ""
     if src.endswith(".cpp"):
         cmd = [HIPCC, "-x", "c++"] + COMMON + ["-c", path, "-o", out]
     else:
@@ -56,11 +65,13 @@ def compile_unit(unit):
     return _run(cmd)
 
 
-def build(jobs=None, verbose=False):
+def build(jobs=None, verbose=False, incremental=False):
+    """Compile every unit (``incremental`` skips objects newer than their
+    sources, for development only) and link the shared library."""
     os.makedirs(BUILD, exist_ok=True)
     jobs = jobs or min(8, os.cpu_count() or 4)
     with ThreadPoolExecutor(max_workers=jobs) as ex:
-        logs = list(ex.map(compile_unit, UNITS))
+        logs = list(ex.map(lambda u: compile_unit(u, incremental), UNITS))
     objs = [os.path.join(BUILD, u[2]) for u in UNITS]
     tmp = LIB + ".tmp"
     link = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}"] + objs + ["-o", tmp]
@@ -77,8 +88,9 @@ def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("-j", "--jobs", type=int, default=None)
     ap.add_argument("-v", "--verbose", action="store_true")
+    ap.add_argument("--incremental", action="store_true", help="skip up-to-date objects (development)")
     a = ap.parse_args(argv)
-    print(build(a.jobs, a.verbose))
+    print(build(a.jobs, a.verbose, a.incremental))
 
 
 if __name__ == "__main__":
