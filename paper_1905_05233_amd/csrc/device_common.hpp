@@ -27,16 +27,10 @@ template <> struct Storage<bf16_t> {
     static __device__ __forceinline__ float to_f32(bf16_t v) {
         return __uint_as_float(static_cast<uint32_t>(v.bits) << 16);
     }
-    // Round to nearest even on the fp32 encoding; NaN stays a quiet NaN.
+    // Round to nearest even (v_cvt_pk_bf16_f32 on gfx950); NaN stays a NaN.
     static __device__ __forceinline__ bf16_t from_f32(float f) {
-        uint32_t u = __float_as_uint(f);
         bf16_t r;
-        if ((u & 0x7fffffffu) > 0x7f800000u) {
-            r.bits = static_cast<uint16_t>((u >> 16) | 0x40u);
-        } else {
-            u += 0x7fffu + ((u >> 16) & 1u);
-            r.bits = static_cast<uint16_t>(u >> 16);
-        }
+        r.bits = __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
         return r;
     }
 };

@@ -28,21 +28,23 @@ namespace {
 constexpr int kBlock = 256;
 
 // ----------------------------------------------------------------- kernel
-// U[xi = a*alpha + b][k][c] = sum_j (sum_i G[a][i] g[i][j]) G[b][j]
+// U[xi = a*alpha + b][k][c] = sum_j (sum_i G[a][i] g[i][j]) G[b][j]; one thread
+// per (row a, k, c), channel fastest.
 template <typename Elem, int ALPHA>
 __global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, const Elem* __restrict__ w,
                                                            Elem* __restrict__ U, int64_t K, int64_t C,
                                                            int64_t Cp) {
     using S = Storage<Elem>;
     const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    if (gid >= K * Cp) return;
+    if (gid >= ALPHA * K * Cp) return;
     const int64_t c = gid % Cp;
-    const int64_t k = gid / Cp;
+    const int64_t k = (gid / Cp) % K;
+    const int a = static_cast<int>(gid / (Cp * K));
     const int64_t plane = K * Cp;
-    Elem* out = U + k * Cp + c;
+    Elem* out = U + static_cast<int64_t>(a) * ALPHA * plane + k * Cp + c;
     if (c >= C) {
 #pragma unroll
-        for (int x = 0; x < ALPHA * ALPHA; ++x) out[x * plane] = S::from_f32(0.0f);
+        for (int b = 0; b < ALPHA; ++b) out[b * plane] = S::from_f32(0.0f);
         return;
     }
     float g[3][3];
@@ -50,25 +52,21 @@ __global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, cons
     for (int i = 0; i < 3; ++i)
 #pragma unroll
         for (int j = 0; j < 3; ++j) g[i][j] = S::to_f32(w[((k * 3 + i) * 3 + j) * C + c]);
-    float Gg[ALPHA][3];
+    float Gg[3];
 #pragma unroll
-    for (int a = 0; a < ALPHA; ++a)
+    for (int j = 0; j < 3; ++j) {
+        float acc = 0.0f;
 #pragma unroll
-        for (int j = 0; j < 3; ++j) {
-            float acc = 0.0f;
+        for (int i = 0; i < 3; ++i) acc = __builtin_fmaf(tab.g[a * 3 + i], g[i][j], acc);
+        Gg[j] = acc;
+    }
 #pragma unroll
-            for (int i = 0; i < 3; ++i) acc = __builtin_fmaf(tab.g[a * 3 + i], g[i][j], acc);
-            Gg[a][j] = acc;
-        }
+    for (int b = 0; b < ALPHA; ++b) {
+        float acc = 0.0f;
 #pragma unroll
-    for (int a = 0; a < ALPHA; ++a)
-#pragma unroll
-        for (int b = 0; b < ALPHA; ++b) {
-            float acc = 0.0f;
-#pragma unroll
-            for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(Gg[a][j], tab.g[b * 3 + j], acc);
-            out[(a * ALPHA + b) * plane] = S::from_f32(acc);
-        }
+        for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(Gg[j], tab.g[b * 3 + j], acc);
+        out[b * plane] = S::from_f32(acc);
+    }
 }
 
 // ------------------------------------------------------------------ input
@@ -144,18 +142,21 @@ __global__ __launch_bounds__(kBlock) void output_transform(OutputTable tab, cons
     const int64_t ty = (tile / geo.tw) % geo.th;
     const int64_t n = tile / (geo.tw * geo.th);
 
+    // every load of the tile's alpha'^2 values is issued before any arithmetic
+    float Mv[ALPHA][ALPHA];
+#pragma unroll
+    for (int a = 0; a < ALPHA; ++a)
+#pragma unroll
+        for (int b = 0; b < ALPHA; ++b) Mv[a][b] = in[(a * ALPHA + b) * plane];
     // pass 1, one domain column at a time: Z[o][b] = sum_a A^T[o][a] M[a][b]
     float Z[MM][ALPHA];
 #pragma unroll
     for (int b = 0; b < ALPHA; ++b) {
-        float col[ALPHA];
-#pragma unroll
-        for (int a = 0; a < ALPHA; ++a) col[a] = in[(a * ALPHA + b) * plane];
 #pragma unroll
         for (int o = 0; o < MM; ++o) {
             float acc = 0.0f;
 #pragma unroll
-            for (int a = 0; a < ALPHA; ++a) acc = __builtin_fmaf(tab.at[o * ALPHA + a], col[a], acc);
+            for (int a = 0; a < ALPHA; ++a) acc = __builtin_fmaf(tab.at[o * ALPHA + a], Mv[a][b], acc);
             Z[o][b] = acc;
         }
     }
@@ -188,7 +189,7 @@ hipError_t launch_kernel_transform_t(const Geometry& g, const KernelTable& tab, 
     using Elem = typename DTypeOf<D>::type;
     const auto* wp = static_cast<const Elem*>(w);
     auto* up = static_cast<Elem*>(U);
-    const unsigned nb = blocks_for(g.K * g.Cp);
+    const unsigned nb = blocks_for(static_cast<int64_t>(g.alpha) * g.K * g.Cp);
     switch (g.alpha) {
 #define WG_KT_CASE(A)                                                                             \
     case A:                                                                                       \
