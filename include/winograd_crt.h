@@ -147,7 +147,7 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
  * index xi = i * alpha' + j:
  *   U [alpha'^2][K][Cp]  dtype, channels Cp > C are zero
  *   V [alpha'^2][T][Cp]  dtype, channels Cp > C are zero
- *   M [alpha'^2][T][Kp]  fp32 (columns K..Kp-1 are not written)          */
+ *   M [alpha'^2][T][Kp]  fp32 (columns K..Kp-1 hold unspecified values)   */
 
 /* U[xi][k][c] = (G g_kc G^T)[i][j]: eq. (2)'s kernel transform. */
 wg_status winograd_kernel_transform(wg_plan plan, const wg_tensor* w, void* U, hipStream_t stream);

@@ -169,23 +169,37 @@ __global__ __launch_bounds__(kThreads, 2) void contract_kernel(const unsigned ch
 // Streaming variant for short reductions (one row of C fits 512 bytes: fp32
 // C <= 128, fp16/bf16 C <= 256), the common DNN case.
 //
-// One persistent 512-thread workgroup per CU walks a contiguous range of work
-// items; an item is 32 rows (tiles) x 128 columns (output channels) of one
-// domain point xi, with the whole reduction.  Items are ordered xi-major, so a
-// workgroup's consecutive items share U[xi]; workgroup ids are remapped so
-// that the ranges of the workgroups of one XCD are adjacent (the hardware
-// hands out consecutive ids round-robin across the 8 XCDs), which keeps each
-// U[xi] in a single L2.  The 8 waves split the item into 2 row halves x 4
-// groups of 32 columns; each wave runs the whole reduction on 16x16 MFMA
-// tiles with four independent accumulators and keeps its U fragments in
-// registers while xi and the column block stay the same (the U block of the
-// next item, when it changes, is fetched one item ahead and parked in LDS).
-// Only the V tile streams: loaded one item ahead into registers and parked in
-// double-buffered LDS, its wait falling after a full MFMA phase.  The 32 x 128
-// block of M is staged in LDS and written with full-row 16-byte stores.
-constexpr int kStreamThreads = 512;
+// One persistent workgroup per CU walks a contiguous range of work items; an
+// item is 32 rows (tiles) x 128 columns (output channels) of one domain point
+// xi, with the whole reduction.  Items are ordered xi-major, so consecutive
+// items share U[xi]; workgroup ids are remapped so that the ranges of the
+// workgroups of one XCD are adjacent (the hardware hands out consecutive ids
+// round-robin across the 8 XCDs), which keeps each U[xi] in a single L2.
+//
+// The workgroup is split by role.  Wave 8, the loader, streams V tiles
+// through registers into double-buffered LDS, two tiles in flight; it issues
+// nothing but loads, so each of its waits covers exactly the tile it needs.
+// Waves 0-7 each own 32 rows x 16 columns of the item: their U fragments stay
+// in registers while the block is unchanged (the next block is fetched one
+// item ahead), A fragments come from LDS, and the finished block of M is
+// stored straight from the accumulators.  These waves issue no global load in
+// the steady state, so their stores are never waited on.  All global accesses
+// go through buffer descriptors whose record counts clip the ragged tails
+// (out-of-range loads return zero, out-of-range stores are dropped).
+constexpr int kStreamMmaWaves = 8;
+constexpr int kStreamThreads = (kStreamMmaWaves + 1) * 64;
 constexpr int kStreamRows = 32;
-constexpr int kStreamCols = 128;
+constexpr int kStreamCols = kStreamMmaWaves * 16;
+constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw 32-bit buffer, gfx9 family
+constexpr uint32_t kOob = 0xfffffff0u;         // an offset beyond every record count used here
+
+// Buffer descriptor over [base, base + bytes), bytes clipped to [0, 2^32 - 1].
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+    const int64_t n = bytes < 0 ? 0 : (bytes > 0xffffffffLL ? 0xffffffffLL : bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                             static_cast<int>(static_cast<uint32_t>(n)),
+                                             static_cast<int>(kRsrcWord3));
+}
 
 template <int D> __device__ __forceinline__ void mma16_chunk(const u32x4& a, const u32x4& b, f32x4& c);
 
@@ -206,51 +220,37 @@ template <> __device__ __forceinline__ void mma16_chunk<2>(const u32x4& a, const
                                                 0, 0, 0);
 }
 
-// One 16-byte chunk of A against the same chunk of two B column blocks.
+// One 16-byte chunk of two 16-row A blocks against the same chunk of one B
+// column block; the two accumulators alternate so consecutive MFMAs are
+// independent.
 template <int D>
-__device__ __forceinline__ void mma16_chunk2(const u32x4& x, const u32x4& y0, const u32x4& y1, f32x4& c0,
-                                             f32x4& c1) {
+__device__ __forceinline__ void mma16_rows2(const u32x4& x0, const u32x4& x1, const u32x4& y, f32x4& c0,
+                                            f32x4& c1) {
     if constexpr (D == 0) {
-        const f32x4 a = __builtin_bit_cast(f32x4, x);
-        const f32x4 b0 = __builtin_bit_cast(f32x4, y0), b1 = __builtin_bit_cast(f32x4, y1);
+        const f32x4 a0 = __builtin_bit_cast(f32x4, x0), a1 = __builtin_bit_cast(f32x4, x1);
+        const f32x4 b = __builtin_bit_cast(f32x4, y);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b0[e], c0, 0, 0, 0);
-            c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b1[e], c1, 0, 0, 0);
+            c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[e], b[e], c0, 0, 0, 0);
+            c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[e], b[e], c1, 0, 0, 0);
         }
     } else {
-        mma16_chunk<D>(x, y0, c0);
-        mma16_chunk<D>(x, y1, c1);
+        mma16_chunk<D>(x0, y, c0);
+        mma16_chunk<D>(x1, y, c1);
     }
 }
 
-template <int NCH>
-struct StreamLds {
-    // NCH = 16-byte chunks per lane per 16-row block: the k range of a row is
-    // 64 * NCH bytes, split over the four 16-lane groups of a wave.
-    static constexpr int kRowBytes = 64 * NCH + 16;                   // + padding: conflict-free reads
-    static constexpr int kABytes = kStreamRows * kRowBytes;           // one V tile (32 rows)
-    static constexpr int kBBytes = kStreamCols * kRowBytes;           // one U block (128 columns)
-    static constexpr int kORowFloats = kStreamCols + 4;               // output staging row (+ padding)
-    static constexpr int kOBytes = kStreamRows * kORowFloats * 4;     // one 32 x 128 fp32 tile of M
-    static constexpr int kUsed = 2 * kABytes + kBBytes + 2 * kOBytes;
-    // at least 84 KB: more than half of a CU's 160 KB, so one workgroup per CU
-    static constexpr int kBytes = kUsed > 84 * 1024 ? kUsed : 84 * 1024;
-    static_assert(kUsed <= 160 * 1024, "LDS layout");
-};
-
-
 template <int D, int NCH>
 __global__ __launch_bounds__(kStreamThreads, 1) void contract_stream_kernel(
-    const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, float* __restrict__ M, int64_t T,
-    int64_t K, int64_t row_bytes, int64_t Kp, int num_mb, int num_nb, int64_t n_items) {
-    using L = StreamLds<NCH>;
-    __shared__ __attribute__((aligned(16))) unsigned char smem[L::kBytes];
-    unsigned char* const abuf = smem;                   // [2][32 rows][kRowBytes]
-    unsigned char* const bbuf = smem + 2 * L::kABytes;  // [128 cols][kRowBytes]
-    float* const obuf = reinterpret_cast<float*>(smem + 2 * L::kABytes + L::kBBytes);  // [2][32][132]
+    const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, unsigned char* __restrict__ M,
+    int64_t T, int64_t K, int rb, int64_t Kp, int num_mb, int num_nb, int64_t n_items) {
+    // NCH = 16-byte chunks per lane per row: the k range of a row (rb <= 64 * NCH
+    // bytes) is split over the four 16-lane groups of a wave.  LDS rows are
+    // padded by one chunk, which keeps the fragment reads conflict-free.
+    constexpr int kRowBytes = 64 * NCH + 16;
+    constexpr int kABytes = kStreamRows * kRowBytes;
+    __shared__ __attribute__((aligned(16))) unsigned char abuf[2 * kABytes];
 
-    // XCD-aware contiguous item range of this workgroup
     const int64_t G = gridDim.x;
     const int64_t bid = blockIdx.x;
     const int64_t v = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
@@ -258,83 +258,13 @@ __global__ __launch_bounds__(kStreamThreads, 1) void contract_stream_kernel(
     const int64_t it1 = (v + 1) * n_items / G;
     if (it0 >= it1) return;
     const int n_mine = static_cast<int>(it1 - it0);
-
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int rh = wave >> 2;              // 16-row half of the item
-    const int cg = wave & 3;               // 32-column group
-    const int grp = lane >> 4;
-    const int l16 = lane & 15;
-    const int kbyte0 = grp * (16 * NCH);   // each 16-lane group owns a quarter of the k range
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-
-    // staging map: chunk ci -> (row, 16-byte column) of a tile row of 64*NCH bytes
-    constexpr int kRowChunks = 4 * NCH;
-    constexpr int kAChunks = kStreamRows * kRowChunks;
-    constexpr int kAPer = (kAChunks + kStreamThreads - 1) / kStreamThreads;
-    constexpr int kBChunks = kStreamCols * kRowChunks;
-    constexpr int kBPer = (kBChunks + kStreamThreads - 1) / kStreamThreads;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
     int xi = static_cast<int>(it0 / (static_cast<int64_t>(num_mb) * num_nb));
     int nb = static_cast<int>((it0 / num_mb) % num_nb);
     int mb = static_cast<int>(it0 % num_mb);
-
-    // U block of (xi, nb): global -> registers, registers -> LDS (all threads;
-    // the caller synchronises around the LDS write)
-    u32x4 breg[kBPer];
-    auto load_b = [&](int bxi, int bnb) {
-        const unsigned char* src = U + static_cast<int64_t>(bxi) * K * row_bytes;
-#pragma unroll
-        for (int p = 0; p < kBPer; ++p) {
-            const int ci = tid + p * kStreamThreads;
-            const int col = ci / kRowChunks;
-            const int c16 = ci % kRowChunks;
-            const int64_t gcol = static_cast<int64_t>(bnb) * kStreamCols + col;
-            const bool ok = ci < kBChunks && gcol < K && c16 * 16 < row_bytes;
-            breg[p] = ok ? *reinterpret_cast<const u32x4*>(src + gcol * row_bytes + c16 * 16) : zero;
-        }
-    };
-    auto store_b = [&]() {
-#pragma unroll
-        for (int p = 0; p < kBPer; ++p) {
-            const int ci = tid + p * kStreamThreads;
-            if (ci < kBChunks)
-                *reinterpret_cast<u32x4*>(bbuf + (ci / kRowChunks) * L::kRowBytes + (ci % kRowChunks) * 16) =
-                    breg[p];
-        }
-    };
-    // V tile rows [mb*32, mb*32+32) of xi -> registers
-    u32x4 areg[kAPer];
-    auto load_a = [&](int axi, int amb) {
-        const unsigned char* src = V + static_cast<int64_t>(axi) * T * row_bytes;
-#pragma unroll
-        for (int p = 0; p < kAPer; ++p) {
-            const int ci = tid + p * kStreamThreads;
-            const int row = ci / kRowChunks;
-            const int c16 = ci % kRowChunks;
-            const int64_t grow = static_cast<int64_t>(amb) * kStreamRows + row;
-            const bool ok = ci < kAChunks && grow < T && c16 * 16 < row_bytes;
-            areg[p] = ok ? *reinterpret_cast<const u32x4*>(src + grow * row_bytes + c16 * 16) : zero;
-        }
-    };
-    auto store_a = [&](int slot) {
-#pragma unroll
-        for (int p = 0; p < kAPer; ++p) {
-            const int ci = tid + p * kStreamThreads;
-            if (ci < kAChunks)
-                *reinterpret_cast<u32x4*>(abuf + slot * L::kABytes + (ci / kRowChunks) * L::kRowBytes +
-                                          (ci % kRowChunks) * 16) = areg[p];
-        }
-    };
-
-    // prologue: first U block and V tile in LDS (loads issued together), the
-    // second V tile in flight
-    load_b(xi, nb);
-    load_a(xi, mb);
-    store_b();
-    store_a(0);
-    int nxi = xi, nnb = nb, nmb = mb;
     auto advance = [&](int& a, int& b, int& c) {
         if (++c == num_mb) {
             c = 0;
@@ -344,91 +274,123 @@ __global__ __launch_bounds__(kStreamThreads, 1) void contract_stream_kernel(
             }
         }
     };
-    advance(nxi, nnb, nmb);
-    if (n_mine > 1) load_a(nxi, nmb);
-    __syncthreads();
 
-    // this wave's U fragments (two 16-column blocks), refreshed from LDS when
-    // the U block changes
-    u32x4 fy0[NCH], fy1[NCH];
-    auto frag_b = [&]() {
-        const unsigned char* b0 = bbuf + (cg * 32 + l16) * L::kRowBytes + kbyte0;
-        const unsigned char* b1 = b0 + 16 * L::kRowBytes;
+    if (wave == kStreamMmaWaves) {
+        // ------------------------------------------------------------ loader
+        constexpr int kRC = 4 * NCH;                      // 16-byte chunks per LDS row
+        constexpr int kLP = kStreamRows * kRC / 64;       // chunks per lane per tile
+        uint32_t voff[kLP];
+        int lofs[kLP];
+#pragma unroll
+        for (int p = 0; p < kLP; ++p) {
+            const int ci = lane + 64 * p;
+            const int row = ci / kRC;
+            const int c16 = ci % kRC;
+            lofs[p] = row * kRowBytes + c16 * 16;
+            voff[p] = c16 * 16 < rb ? static_cast<uint32_t>(row * rb + c16 * 16) : kOob;   // zero past the row
+        }
+        u32x4 s0[kLP], s1[kLP];
+        int lxi = xi, lnb = nb, lmb = mb;   // next tile to request
+        auto load = [&](u32x4 (&s)[kLP]) {
+            const int64_t r0 = static_cast<int64_t>(lmb) * kStreamRows;
+            const auto r = make_rsrc(V + (static_cast<int64_t>(lxi) * T + r0) * rb, (T - r0) * rb);
+#pragma unroll
+            for (int p = 0; p < kLP; ++p) s[p] = __builtin_amdgcn_raw_buffer_load_b128(r, voff[p], 0, 0);
+            advance(lxi, lnb, lmb);
+        };
+        auto park = [&](const u32x4 (&s)[kLP], int slot) {
+#pragma unroll
+            for (int p = 0; p < kLP; ++p) *reinterpret_cast<u32x4*>(abuf + slot * kABytes + lofs[p]) = s[p];
+        };
+        load(s0);
+        if (n_mine > 1) load(s1);
+        park(s0, 0);
+        if (n_mine > 2) load(s0);
+        __syncthreads();
+        // during item i: park tile i+1, request tile i+3 in its registers
+        for (int i = 0; i < n_mine; i += 2) {
+            if (i + 1 < n_mine) {
+                park(s1, 1);
+                if (i + 3 < n_mine) load(s1);
+            }
+            __syncthreads();
+            if (i + 1 >= n_mine) break;
+            if (i + 2 < n_mine) {
+                park(s0, 0);
+                if (i + 4 < n_mine) load(s0);
+            }
+            __syncthreads();
+        }
+        return;
+    }
+
+    // -------------------------------------------------------------- MFMA waves
+    const int grp = lane >> 4;
+    const int l16 = lane & 15;
+    const int kb0 = grp * (16 * NCH);   // each 16-lane group owns a quarter of the k range
+    u32x4 fy[NCH], fyn[NCH];
+    auto load_b = [&](u32x4 (&dst)[NCH], int bxi, int bnb) {
+        const int64_t c0 = static_cast<int64_t>(bnb) * kStreamCols;
+        const auto r = make_rsrc(U + (static_cast<int64_t>(bxi) * K + c0) * rb, (K - c0) * rb);
+        const uint32_t col = static_cast<uint32_t>((wave * 16 + l16) * rb);
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            fy0[c] = *reinterpret_cast<const u32x4*>(b0 + c * 16);
-            fy1[c] = *reinterpret_cast<const u32x4*>(b1 + c * 16);
+            const int byte = kb0 + c * 16;
+            dst[c] = __builtin_amdgcn_raw_buffer_load_b128(r, byte < rb ? col + byte : kOob, 0, 0);
         }
     };
-    frag_b();
+    // the wait for the U fragments lands here, outside the MFMA phase
+    auto settle = [&]() {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) asm volatile("" : "+v"(fy[c]));
+    };
+    load_b(fy, xi, nb);
+    settle();
+    int nxi = xi, nnb = nb, nmb = mb;
+    advance(nxi, nnb, nmb);
+    __syncthreads();
 
+    // 16x16 accumulator layout: lane holds column l16, rows 4*grp + q
+    const uint32_t m_row = static_cast<uint32_t>(Kp * 4);
+    const uint32_t m_lane = static_cast<uint32_t>((4 * grp * Kp + wave * 16 + l16) * 4);
+    const unsigned char* arow = abuf + l16 * kRowBytes + kb0;
     int slot = 0;
     for (int i = 0; i < n_mine; ++i) {
-        // the next item's U block, if it changes, is fetched during this item
+        // the next item's U block, when it changes, arrives during this item
         const bool new_b = i + 1 < n_mine && (nxi != xi || nnb != nb);
-        if (new_b) load_b(nxi, nnb);
-        // 16 rows x 32 columns of this wave: four accumulators (two column
-        // blocks x even/odd chunks) so consecutive MFMAs are independent
-        f32x4 acc[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) acc[q] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        const unsigned char* arow = abuf + slot * L::kABytes + (rh * 16 + l16) * L::kRowBytes + kbyte0;
-        u32x4 fx[NCH];
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) fx[c] = *reinterpret_cast<const u32x4*>(arow + c * 16);
+        if (new_b) load_b(fyn, nxi, nnb);
+        f32x4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
+        const unsigned char* a = arow + slot * kABytes;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            const int q = c & 1;
-            mma16_chunk2<D>(fx[c], fy0[c], fy1[c], acc[q], acc[2 + q]);
+            const u32x4 x0 = *reinterpret_cast<const u32x4*>(a + c * 16);
+            const u32x4 x1 = *reinterpret_cast<const u32x4*>(a + 16 * kRowBytes + c * 16);
+            mma16_rows2<D>(x0, x1, fy[c], acc0, acc1);
         }
-        const bool has_next = i + 1 < n_mine;
-        // park the next item's V tile (in flight since the previous item)
-        if (has_next) store_a(slot ^ 1);
-        // stage the 32 x 128 block of M in LDS (16x16 accumulator layout: lane
-        // holds column l16, rows 4*grp + r of each 16-row block)
-        float* ob = obuf + slot * (L::kOBytes / 4);
+        if (new_b) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            float* orow = ob + (rh * 16 + 4 * grp + r) * L::kORowFloats + cg * 32 + l16;
-            orow[0] = acc[0][r] + acc[1][r];
-            orow[16] = acc[2][r] + acc[3][r];
+            for (int c = 0; c < NCH; ++c) fy[c] = fyn[c];
+            settle();
         }
-        __syncthreads();
-        // full-row 16-byte stores: 32 rows x 32 chunks of 4 floats
         {
-            float* Mx = M + static_cast<int64_t>(xi) * T * Kp;
-            const int64_t col0 = static_cast<int64_t>(nb) * kStreamCols;
+            const int64_t r0 = static_cast<int64_t>(mb) * kStreamRows;
+            const int64_t c0 = static_cast<int64_t>(nb) * kStreamCols;
+            const auto r = make_rsrc(M + ((static_cast<int64_t>(xi) * T + r0) * Kp + c0) * 4,
+                                     (T - r0) * Kp * 4 - c0 * 4);
+            const bool ok = c0 + wave * 16 + l16 < Kp;   // columns past Kp would wrap into the next row
 #pragma unroll
-            for (int p = 0; p < 2; ++p) {
-                const int ci = tid + p * kStreamThreads;
-                const int row = ci >> 5;
-                const int c4 = (ci & 31) * 4;
-                const int64_t grow = static_cast<int64_t>(mb) * kStreamRows + row;
-                const int64_t gcol = col0 + c4;
-                if (grow < T && gcol < K) {
-                    const f32x4 val = *reinterpret_cast<const f32x4*>(ob + row * L::kORowFloats + c4);
-                    float* dst = Mx + grow * Kp + gcol;
-                    if (gcol + 4 <= Kp) {
-                        *reinterpret_cast<f32x4*>(dst) = val;
-                    } else {
-                        for (int e = 0; e < 4 && gcol + e < K; ++e) dst[e] = val[e];
-                    }
-                }
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t off = m_lane + q * m_row;
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc0[q]), r, ok ? off : kOob, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc1[q]), r, ok ? off + 16 * m_row : kOob,
+                                                      0, 0);
             }
         }
-        if (has_next) {
-            xi = nxi;
-            nb = nnb;
-            mb = nmb;
-            advance(nxi, nnb, nmb);
-            if (new_b) {
-                // all waves are past their reads of the old block (barrier above)
-                store_b();
-                __syncthreads();
-                frag_b();
-            }
-            if (i + 2 < n_mine) load_a(nxi, nmb);
-        }
+        xi = nxi;
+        nb = nnb;
+        mb = nmb;
+        advance(nxi, nnb, nmb);
+        __syncthreads();
         slot ^= 1;
     }
 }
@@ -453,8 +415,9 @@ hipError_t launch_stream(const Geometry& g, const void* V, const void* U, float*
     const int64_t n_items = static_cast<int64_t>(num_mb) * num_nb * g.alpha * g.alpha;
     const int64_t grid = std::min<int64_t>(n_items, device_cu_count());
     hipLaunchKernelGGL((contract_stream_kernel<D, NCH>), dim3(static_cast<unsigned>(grid)), dim3(kStreamThreads), 0,
-                       stream, static_cast<const unsigned char*>(V), static_cast<const unsigned char*>(U), M, g.T,
-                       g.K, row_bytes, g.Kp, num_mb, num_nb, n_items);
+                       stream, static_cast<const unsigned char*>(V), static_cast<const unsigned char*>(U),
+                       reinterpret_cast<unsigned char*>(M), g.T, g.K, static_cast<int>(row_bytes), g.Kp, num_mb,
+                       num_nb, n_items);
     return hipGetLastError();
 }
 
@@ -464,10 +427,13 @@ template <int D>
 hipError_t launch_contract_t(const Geometry& g, const void* V, const void* U, float* M, hipStream_t stream) {
     const int64_t es = D == 0 ? 4 : 2;
     const int64_t row_bytes = g.Cp * es;
-    if (row_bytes <= 64) return launch_stream<D, 1>(g, V, U, M, row_bytes, stream);
-    if (row_bytes <= 128) return launch_stream<D, 2>(g, V, U, M, row_bytes, stream);
-    if (row_bytes <= 256) return launch_stream<D, 4>(g, V, U, M, row_bytes, stream);
-    if (row_bytes <= 512) return launch_stream<D, 8>(g, V, U, M, row_bytes, stream);
+    // the streaming kernel addresses each plane of V, U and M with 32-bit offsets
+    const bool fits32 = g.T * row_bytes < 0xffff0000LL && g.K * row_bytes < 0xffff0000LL &&
+                        g.T * g.Kp * 4 < 0xffff0000LL;
+    if (fits32 && row_bytes <= 64) return launch_stream<D, 1>(g, V, U, M, row_bytes, stream);
+    if (fits32 && row_bytes <= 128) return launch_stream<D, 2>(g, V, U, M, row_bytes, stream);
+    if (fits32 && row_bytes <= 256) return launch_stream<D, 4>(g, V, U, M, row_bytes, stream);
+    if (fits32 && row_bytes <= 512) return launch_stream<D, 8>(g, V, U, M, row_bytes, stream);
     const int num_mb = static_cast<int>((g.T + kBM - 1) / kBM);
     const int num_nb = static_cast<int>((g.K + kBN - 1) / kBN);
     const int64_t blocks = static_cast<int64_t>(num_mb) * num_nb * g.alpha * g.alpha;
