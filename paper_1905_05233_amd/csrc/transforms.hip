@@ -2,18 +2,22 @@
 // gfx950: the kernel transform U = G g G^T, the input transform V = B^T d B
 // and the output transform Y = A^T M A fused with the NHWC store.
 //
-// All three are memory-bound.  Each thread owns one (tile, channel) or
-// (kernel, channel) pair, so a wavefront's loads and stores sweep 64
-// consecutive channels of NHWC / channel-last buffers (coalesced).  The
-// transform matrices arrive by value in the kernel-argument segment (they are
-// uniform across the grid and live in scalar registers); the small matrices
-// are applied as two separable 1D passes in fp32 registers with ascending-index
-// fused multiply-adds, and results are rounded to the storage dtype once, at
-// the store.
+// All three stream channel-last data: a wavefront's loads and stores sweep 64
+// consecutive channels of NHWC / channel-last buffers (coalesced).  The kernel
+// transform runs one thread per (domain row, kernel, channel), the input
+// transform one workgroup per (tile, 64 channels) with its window staged in
+// LDS and its domain rows split over the waves, the output transform one
+// thread per (tile, output channel).  The transform matrices arrive by value
+// in the kernel-argument segment (uniform across the grid, so they live in
+// scalar registers); the small matrices are applied as two separable 1D passes
+// in fp32 registers with ascending-index fused multiply-adds, and results are
+// rounded to the storage dtype once, at the store.
 //
 // This file is compiled once per storage dtype (WG_DTYPE = 0 fp32, 1 fp16,
 // 2 bf16); each (input tile, alpha') shape is a template instance so that the
 // register arrays have compile-time sizes.
+#include <utility>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -72,58 +76,130 @@ __global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, cons
 // ------------------------------------------------------------------ input
 // V[xi = a*alpha + b][tile][c] = sum_v (sum_u B^T[a][u] d[u][v]) B^T[b][v],
 // d = the (m+2)^2 window whose top-left pixel is (ty*m - 1, tx*m - 1).
+//
+// One workgroup per (tile, 64 channels).  The t x t x 64 window (neighbouring
+// tiles overlap by two pixels) is fetched with coalesced 16-byte NHWC loads,
+// zero outside the image and past C, converted to fp32 once and staged in
+// LDS.  The alpha' output rows are split over the waves: wave g computes rows
+// [g*R, g*R + R) for its 64 channels, so each wave runs both passes for few
+// rows and the workgroup's VALU work is spread over several waves.  Row
+// indices are compile-time constants in every wave (one template instance per
+// row group), which keeps the coefficients in scalar registers.
+constexpr int kInCh = 64;   // channels per workgroup, one per lane
+
+// rows per wave: the split that measured fastest for each alpha'
+constexpr int input_rows_per_wave(int alpha) { return alpha == 7 || alpha == 8 ? 2 : 3; }
+
 template <typename Elem, int TT, int ALPHA>
-__global__ __launch_bounds__(kBlock) void input_transform(InputTable tab, const Elem* __restrict__ x,
-                                                          Elem* __restrict__ V, Geometry geo) {
+struct InputShape {
+    static constexpr int kR = input_rows_per_wave(ALPHA);
+    static constexpr int kG = (ALPHA + kR - 1) / kR;                  // waves (row groups)
+    static constexpr int kThreads = 64 * kG;
+    static constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
+    static constexpr int kChunksPerPix = kInCh / kChunkElems;
+    static constexpr int kChunks = TT * TT * kChunksPerPix;            // 16-byte chunks per window
+    static constexpr int kPer = (kChunks + kThreads - 1) / kThreads;
+};
+
+// Both passes for rows A0 .. A0+R-1 of one (tile, channel): pass 1 in ascending
+// u, pass 2 in ascending v, rounded to the storage type at the store.
+template <typename Elem, int TT, int ALPHA, int R, int A0>
+__device__ __forceinline__ void input_rows(const InputTable& tab, const float* wb, Elem* __restrict__ out,
+                                           int64_t plane) {
     using S = Storage<Elem>;
-    const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    if (gid >= geo.T * geo.Cp) return;
-    const int64_t c = gid % geo.Cp;
-    const int64_t tile = gid / geo.Cp;
-    const int64_t plane = geo.T * geo.Cp;
-    Elem* out = V + tile * geo.Cp + c;
-    if (c >= geo.C) {
+    float W1[R][TT];
 #pragma unroll
-        for (int xi = 0; xi < ALPHA * ALPHA; ++xi) out[xi * plane] = S::from_f32(0.0f);
-        return;
+    for (int v = 0; v < TT; ++v) {
+        float col[TT];
+#pragma unroll
+        for (int u = 0; u < TT; ++u) col[u] = wb[(u * TT + v) * kInCh];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            float acc = 0.0f;
+            if (A0 + r < ALPHA) {
+#pragma unroll
+                for (int u = 0; u < TT; ++u) acc = __builtin_fmaf(tab.bt[(A0 + r) * TT + u], col[u], acc);
+            }
+            W1[r][v] = acc;
+        }
     }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        if (A0 + r >= ALPHA) break;
+#pragma unroll
+        for (int b = 0; b < ALPHA; ++b) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int v = 0; v < TT; ++v) acc = __builtin_fmaf(W1[r][v], tab.bt[b * TT + v], acc);
+            out[((A0 + r) * ALPHA + b) * plane] = S::from_f32(acc);
+        }
+    }
+}
+
+template <typename Elem, int TT, int ALPHA, int R, int... Gs>
+__device__ __forceinline__ void input_row_groups(int g, const InputTable& tab, const float* wb, Elem* out,
+                                                 int64_t plane, std::integer_sequence<int, Gs...>) {
+    ((g == Gs ? (input_rows<Elem, TT, ALPHA, R, Gs * R>(tab, wb, out, plane), 0) : 0), ...);
+}
+
+// kWhole: C is a multiple of the 16-byte chunk width, so a chunk lies wholly
+// inside or wholly past C; otherwise the window is fetched element by element.
+template <typename Elem, int TT, int ALPHA, bool kWhole>
+__global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input_transform(
+    InputTable tab, const Elem* __restrict__ x, Elem* __restrict__ V, Geometry geo) {
+    using S = Storage<Elem>;
+    using P = InputShape<Elem, TT, ALPHA>;
+    __shared__ __attribute__((aligned(16))) float win[TT * TT * kInCh];   // [u][v][64] fp32
+
+    const int64_t nch = (geo.Cp + kInCh - 1) / kInCh;
+    const int64_t unit = blockIdx.x;
+    const int64_t tile = unit / nch;
+    const int64_t c0 = (unit % nch) * kInCh;
     const int64_t tx = tile % geo.tw;
     const int64_t ty = (tile / geo.tw) % geo.th;
     const int64_t n = tile / (geo.tw * geo.th);
     const int64_t h0 = ty * geo.m - 1;
     const int64_t w0 = tx * geo.m - 1;
-    const Elem* xn = x + n * geo.H * geo.W * geo.C + c;
+    const Elem* xn = x + n * geo.H * geo.W * geo.C;
+    const int tid = threadIdx.x;
 
-    // pass 1, one input column at a time: W1[a][v] = sum_u B^T[a][u] d[u][v]
-    float W1[ALPHA][TT];
+    uint4 regs[P::kPer];
 #pragma unroll
-    for (int v = 0; v < TT; ++v) {
-        const int64_t wc = w0 + v;
-        const bool col_ok = wc >= 0 && wc < geo.W;
-        float col[TT];
+    for (int p = 0; p < P::kPer; ++p) {
+        const int ci = tid + p * P::kThreads;
+        const int pix = ci / P::kChunksPerPix;
+        const int64_t hr = h0 + pix / TT;
+        const int64_t wc = w0 + pix % TT;
+        const int64_t cc = c0 + (ci % P::kChunksPerPix) * P::kChunkElems;
+        const bool in = ci < P::kChunks && hr >= 0 && hr < geo.H && wc >= 0 && wc < geo.W;
+        const Elem* src = xn + (hr * geo.W + wc) * geo.C + cc;
+        if constexpr (kWhole) {
+            regs[p] = (in && cc < geo.C) ? *reinterpret_cast<const uint4*>(src) : uint4{0u, 0u, 0u, 0u};
+        } else {
+            Elem e[P::kChunkElems];
 #pragma unroll
-        for (int u = 0; u < TT; ++u) {
-            const int64_t hr = h0 + u;
-            col[u] = (col_ok && hr >= 0 && hr < geo.H) ? S::to_f32(xn[(hr * geo.W + wc) * geo.C]) : 0.0f;
-        }
-#pragma unroll
-        for (int a = 0; a < ALPHA; ++a) {
-            float acc = 0.0f;
-#pragma unroll
-            for (int u = 0; u < TT; ++u) acc = __builtin_fmaf(tab.bt[a * TT + u], col[u], acc);
-            W1[a][v] = acc;
+            for (int k = 0; k < P::kChunkElems; ++k) e[k] = (in && cc + k < geo.C) ? src[k] : S::from_f32(0.0f);
+            regs[p] = __builtin_bit_cast(uint4, e);
         }
     }
-    // pass 2, one output row at a time: V[a][b] = sum_v W1[a][v] B^T[b][v]
 #pragma unroll
-    for (int a = 0; a < ALPHA; ++a)
+    for (int p = 0; p < P::kPer; ++p) {
+        const int ci = tid + p * P::kThreads;
+        if (ci < P::kChunks) {
+            const Elem* e = reinterpret_cast<const Elem*>(&regs[p]);
 #pragma unroll
-        for (int b = 0; b < ALPHA; ++b) {
-            float acc = 0.0f;
-#pragma unroll
-            for (int v = 0; v < TT; ++v) acc = __builtin_fmaf(W1[a][v], tab.bt[b * TT + v], acc);
-            out[(a * ALPHA + b) * plane] = S::from_f32(acc);
+            for (int k = 0; k < P::kChunkElems; ++k) win[ci * P::kChunkElems + k] = S::to_f32(e[k]);
         }
+    }
+    __syncthreads();
+
+    const int c = tid % kInCh;
+    const int g = __builtin_amdgcn_readfirstlane(tid / kInCh);
+    const int64_t cg = c0 + c;
+    if (cg >= geo.Cp) return;
+    // channels C..Cp-1 read as zero and so store zeros
+    input_row_groups<Elem, TT, ALPHA, P::kR>(g, tab, win + c, V + tile * geo.Cp + cg, geo.T * geo.Cp,
+                                             std::make_integer_sequence<int, P::kG>{});
 }
 
 // ----------------------------------------------------------------- output
@@ -212,11 +288,19 @@ hipError_t launch_input_transform_t(const Geometry& g, const InputTable& tab, co
     using Elem = typename DTypeOf<D>::type;
     const auto* xp = static_cast<const Elem*>(x);
     auto* vp = static_cast<Elem*>(V);
-    const unsigned nb = blocks_for(g.T * g.Cp);
-#define WG_IT_CASE(TT, A)                                                                               \
-    if (g.t == TT && g.alpha == A) {                                                                    \
-        hipLaunchKernelGGL((input_transform<Elem, TT, A>), dim3(nb), dim3(kBlock), 0, stream, tab, xp, vp, g); \
-        return hipGetLastError();                                                                       \
+    constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
+    const bool whole = g.C % kChunkElems == 0;
+    const int64_t units = g.T * ((g.Cp + kInCh - 1) / kInCh);
+    if (units > 0x7fffffff) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(units));
+#define WG_IT_CASE(TT, A)                                                                                  \
+    if (g.t == TT && g.alpha == A) {                                                                       \
+        const dim3 block(InputShape<Elem, TT, A>::kThreads);                                               \
+        if (whole)                                                                                         \
+            hipLaunchKernelGGL((input_transform<Elem, TT, A, true>), grid, block, 0, stream, tab, xp, vp, g); \
+        else                                                                                               \
+            hipLaunchKernelGGL((input_transform<Elem, TT, A, false>), grid, block, 0, stream, tab, xp, vp, g); \
+        return hipGetLastError();                                                                          \
     }
     WG_TRANSFORM_SHAPES(WG_IT_CASE)
 #undef WG_IT_CASE
