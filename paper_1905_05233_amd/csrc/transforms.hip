@@ -152,7 +152,12 @@ __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input
     __shared__ __attribute__((aligned(16))) float win[TT * TT * kInCh];   // [u][v][64] fp32
 
     const int64_t nch = (geo.Cp + kInCh - 1) / kInCh;
-    const int64_t unit = blockIdx.x;
+    // XCD-aware numbering: the hardware deals workgroup ids round-robin to the
+    // 8 XCDs; giving each XCD a contiguous run of units keeps neighbouring
+    // tiles, whose windows overlap, in the same L2
+    const int64_t G = gridDim.x;
+    const int64_t bid = blockIdx.x;
+    const int64_t unit = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
     const int64_t tile = unit / nch;
     const int64_t c0 = (unit % nch) * kInCh;
     const int64_t tx = tile % geo.tw;
