@@ -7,7 +7,8 @@
 // transform runs one thread per (domain row, kernel, channel), the input
 // transform one workgroup per (tile, 64 channels) with its window staged in
 // LDS and its domain rows split over the waves, the output transform one
-// thread per (tile, output channel).  The transform matrices arrive by value
+// workgroup per (tile, 64 output channels) with its output rows split over
+// the waves.  The transform matrices arrive by value
 // in the kernel-argument segment (uniform across the grid, so they live in
 // scalar registers); the small matrices are applied as two separable 1D passes
 // in fp32 registers with ascending-index fused multiply-adds, and results are
@@ -209,53 +210,90 @@ __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input
 
 // ----------------------------------------------------------------- output
 // y[n][ty*m+o][tx*m+p][k] = sum_b (sum_a A^T[o][a] M[a][b]) A^T[p][b]
-template <typename Elem, int MM, int ALPHA>
-__global__ __launch_bounds__(kBlock) void output_transform(OutputTable tab, const float* __restrict__ Mx,
-                                                           Elem* __restrict__ y, Geometry geo) {
-    using S = Storage<Elem>;
-    const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    if (gid >= geo.T * geo.K) return;
-    const int64_t k = gid % geo.K;
-    const int64_t tile = gid / geo.K;
-    const int64_t plane = geo.T * geo.Kp;
-    const float* in = Mx + tile * geo.Kp + k;
-    const int64_t tx = tile % geo.tw;
-    const int64_t ty = (tile / geo.tw) % geo.th;
-    const int64_t n = tile / (geo.tw * geo.th);
+//
+// One workgroup per (tile, 64 output channels); the m output rows are split
+// over its waves (wave g computes rows [g*R, g*R + R) for its 64 channels).
+// Every wave loads the tile's alpha'^2 values of M for its channels, all
+// before any arithmetic (coalesced 256-byte rows; the repeats across the
+// workgroup's waves are served by the caches), then runs pass 1 in ascending
+// a and pass 2 in ascending b and stores its rows, masked at the right and
+// bottom edges of the image.
+constexpr int kOutCh = 64;   // output channels per workgroup, one per lane
 
-    // every load of the tile's alpha'^2 values is issued before any arithmetic
+// rows per wave: the split that measured fastest
+constexpr int output_rows_per_wave(int alpha) { return alpha >= 9 ? 3 : 2; }
+
+template <int MM, int ALPHA>
+struct OutputShape {
+    static constexpr int kR = output_rows_per_wave(ALPHA);
+    static constexpr int kG = (MM + kR - 1) / kR;   // waves (row groups)
+    static constexpr int kThreads = 64 * kG;
+};
+
+template <typename Elem, int MM, int ALPHA, int O0>
+__device__ __forceinline__ void output_rows(const OutputTable& tab, const float* __restrict__ in, int64_t plane,
+                                            Elem* __restrict__ yk, int64_t hr0, int64_t wc0, const Geometry& geo) {
+    using S = Storage<Elem>;
+    constexpr int R = OutputShape<MM, ALPHA>::kR;
     float Mv[ALPHA][ALPHA];
 #pragma unroll
     for (int a = 0; a < ALPHA; ++a)
 #pragma unroll
         for (int b = 0; b < ALPHA; ++b) Mv[a][b] = in[(a * ALPHA + b) * plane];
-    // pass 1, one domain column at a time: Z[o][b] = sum_a A^T[o][a] M[a][b]
-    float Z[MM][ALPHA];
+    // pass 1, one domain column at a time: Z[r][b] = sum_a A^T[O0+r][a] M[a][b]
+    float Z[R][ALPHA];
 #pragma unroll
-    for (int b = 0; b < ALPHA; ++b) {
+    for (int b = 0; b < ALPHA; ++b)
 #pragma unroll
-        for (int o = 0; o < MM; ++o) {
+        for (int r = 0; r < R; ++r) {
             float acc = 0.0f;
+            if (O0 + r < MM) {
 #pragma unroll
-            for (int a = 0; a < ALPHA; ++a) acc = __builtin_fmaf(tab.at[o * ALPHA + a], Mv[a][b], acc);
-            Z[o][b] = acc;
+                for (int a = 0; a < ALPHA; ++a) acc = __builtin_fmaf(tab.at[(O0 + r) * ALPHA + a], Mv[a][b], acc);
+            }
+            Z[r][b] = acc;
         }
-    }
     // pass 2 and the masked NHWC store
-    Elem* yn = y + n * geo.H * geo.W * geo.K + k;
 #pragma unroll
-    for (int o = 0; o < MM; ++o) {
-        const int64_t hr = ty * MM + o;
-        if (hr >= geo.H) break;
+    for (int r = 0; r < R; ++r) {
+        const int64_t hr = hr0 + O0 + r;
+        if (O0 + r >= MM || hr >= geo.H) break;
 #pragma unroll
         for (int p = 0; p < MM; ++p) {
-            const int64_t wc = tx * MM + p;
+            const int64_t wc = wc0 + p;
             float acc = 0.0f;
 #pragma unroll
-            for (int b = 0; b < ALPHA; ++b) acc = __builtin_fmaf(Z[o][b], tab.at[p * ALPHA + b], acc);
-            if (wc < geo.W) yn[(hr * geo.W + wc) * geo.K] = S::from_f32(acc);
+            for (int b = 0; b < ALPHA; ++b) acc = __builtin_fmaf(Z[r][b], tab.at[p * ALPHA + b], acc);
+            if (wc < geo.W) yk[(hr * geo.W + wc) * geo.K] = S::from_f32(acc);
         }
     }
+}
+
+template <typename Elem, int MM, int ALPHA, int... Gs>
+__device__ __forceinline__ void output_row_groups(int g, const OutputTable& tab, const float* in, int64_t plane,
+                                                  Elem* yk, int64_t hr0, int64_t wc0, const Geometry& geo,
+                                                  std::integer_sequence<int, Gs...>) {
+    ((g == Gs ? (output_rows<Elem, MM, ALPHA, Gs * OutputShape<MM, ALPHA>::kR>(tab, in, plane, yk, hr0, wc0, geo),
+                 0)
+              : 0),
+     ...);
+}
+
+template <typename Elem, int MM, int ALPHA>
+__global__ __launch_bounds__((OutputShape<MM, ALPHA>::kThreads)) void output_transform(
+    OutputTable tab, const float* __restrict__ Mx, Elem* __restrict__ y, Geometry geo) {
+    const int64_t nkc = (geo.K + kOutCh - 1) / kOutCh;
+    const int64_t unit = blockIdx.x;
+    const int64_t tile = unit / nkc;
+    const int64_t k = (unit % nkc) * kOutCh + threadIdx.x % kOutCh;
+    const int g = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kOutCh);
+    if (k >= geo.K) return;
+    const int64_t tx = tile % geo.tw;
+    const int64_t ty = (tile / geo.tw) % geo.th;
+    const int64_t n = tile / (geo.tw * geo.th);
+    output_row_groups<Elem, MM, ALPHA>(g, tab, Mx + tile * geo.Kp + k, geo.T * geo.Kp,
+                                       y + n * geo.H * geo.W * geo.K + k, ty * MM, tx * MM, geo,
+                                       std::make_integer_sequence<int, OutputShape<MM, ALPHA>::kG>{});
 }
 
 inline unsigned blocks_for(int64_t n) { return static_cast<unsigned>((n + kBlock - 1) / kBlock); }
@@ -317,11 +355,14 @@ hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, 
                                      hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
     auto* yp = static_cast<Elem*>(y);
-    const unsigned nb = blocks_for(g.T * g.K);
-#define WG_OT_CASE(TT, A)                                                                                   \
-    if (g.t == TT && g.alpha == A) {                                                                        \
-        hipLaunchKernelGGL((output_transform<Elem, TT - 2, A>), dim3(nb), dim3(kBlock), 0, stream, tab, M, yp, g); \
-        return hipGetLastError();                                                                           \
+    const int64_t units = g.T * ((g.K + kOutCh - 1) / kOutCh);
+    if (units > 0x7fffffff) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(units));
+#define WG_OT_CASE(TT, A)                                                                                    \
+    if (g.t == TT && g.alpha == A) {                                                                         \
+        hipLaunchKernelGGL((output_transform<Elem, TT - 2, A>), grid, dim3(OutputShape<TT - 2, A>::kThreads), 0, \
+                           stream, tab, M, yp, g);                                                           \
+        return hipGetLastError();                                                                            \
     }
     WG_TRANSFORM_SHAPES(WG_OT_CASE)
 #undef WG_OT_CASE
