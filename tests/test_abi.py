@@ -28,6 +28,8 @@ PLAN_SETS = [
     ("0,a^3+2", 2, "0,-1,1,-2,inf"), ("0,1,-1,2,-2,inf", 4, "0,-1,inf"),
     ("0,-1,1,-1/2,2,1/2,-2,a^2+1,inf", 8, "0,-1,inf"),
     ("0,-1,1,-1/2,2,1/2,-2,-1/4,4,a^2+1,inf", 10, "0,-1,inf"),
+    ("0,1,-1,1/2,-1/2,2,-2,1/4,-4,4,-1/4,a^2+1,inf", 12, "0,-1,inf"),
+    ("0,-1,a^3+2,inf", 4, "0,-1,1,-2,inf"), ("0,1,-1,1/2,-1/2,2", 4, "0,-1,inf"),
 ]
 
 
