@@ -13,6 +13,10 @@ roofline of the dominant kernel, the rel-L2 error against fp64 direct
 convolution, and the CPU oracle's throughput on the same workload.
 
     python bench.py [--steps K] [--warmup W] [--workload cfg2] [--plan 0]
+
+``--workload cfg5`` runs the VGG-16-shaped stack instead (thirteen layers at
+N = 32, ``--dtype`` bf16 or f16, the most accurate candidate plan per layer);
+its step is one pass through the thirteen convolutions.
 """
 import argparse
 import ctypes
@@ -68,6 +72,165 @@ def load_traffic(kernel, workload_tag):
     return rec.get("hbm_bytes_per_launch")
 
 
+def make_stages(plan, xd, wd, y, N_, H, W, C, K, stream):
+    """Launchers of the four stage kernels of one layer (intermediates
+    allocated here), each returning the library's status."""
+    import torch
+    from paper_1905_05233_amd import _native as NAT
+    lib = NAT.lib()
+    g = plan.geometry(N_, H, W, C, K)
+    a2 = plan.alpha ** 2
+    dev = xd.device
+    U = torch.empty((a2, K, g["Cp"]), dtype=xd.dtype, device=dev)
+    V = torch.empty((a2, g["T"], g["Cp"]), dtype=xd.dtype, device=dev)
+    M = torch.empty((a2, g["T"], g["Kp"]), dtype=torch.float32, device=dev)
+    xt = NAT.WgTensor(ctypes.c_void_p(xd.data_ptr()), N_, H, W, C)
+    wt = NAT.WgTensor(ctypes.c_void_p(wd.data_ptr()), K, 3, 3, C)
+    yt = NAT.WgTensor(ctypes.c_void_p(y.data_ptr()), N_, H, W, K)
+    sh = ctypes.c_void_p(stream.cuda_stream)
+    # the closures keep U, V, M and the tensor descriptors alive
+    return {
+        "kernel_transform": lambda: lib.winograd_kernel_transform(plan._h, ctypes.byref(wt),
+                                                                  ctypes.c_void_p(U.data_ptr()), sh),
+        "input_transform": lambda: lib.winograd_input_transform(plan._h, ctypes.byref(xt),
+                                                                ctypes.c_void_p(V.data_ptr()), sh),
+        "contract": lambda: lib.winograd_contract(plan._h, ctypes.c_void_p(V.data_ptr()),
+                                                  ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(M.data_ptr()),
+                                                  g["T"], C, K, sh),
+        "output_transform": lambda: lib.winograd_output_transform(plan._h, ctypes.c_void_p(M.data_ptr()),
+                                                                  ctypes.byref(yt), sh),
+    }
+
+
+def time_kernels(stages, reps, stream):
+    """Average duration (us) of each stage kernel over ``reps`` back-to-back
+    launches on ``stream``, bracketed by HIP events."""
+    import torch
+    from paper_1905_05233_amd import _native as NAT
+    for name in KERNEL_NAMES:
+        NAT.check(stages[name]())
+    torch.cuda.synchronize()
+    out = {}
+    for name in KERNEL_NAMES:
+        fn = stages[name]
+        for _ in range(3):
+            fn()
+        k0 = torch.cuda.Event(enable_timing=True)
+        k1 = torch.cuda.Event(enable_timing=True)
+        k0.record(stream)
+        for _ in range(reps):
+            fn()
+        k1.record(stream)
+        torch.cuda.synchronize()
+        out[name] = 1e3 * k0.elapsed_time(k1) / reps
+    return out
+
+
+def roofline(dom, work, us, dtype):
+    """Roofline record of kernel ``dom`` from its algorithmic work and time."""
+    if dom == "contract":
+        ai = work["flops"] / work["bytes"]
+        ridge = MFMA_PEAK_TFLOPS[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+        if ai >= ridge:
+            roof = {"bound": "mfma", "achieved": round(work["flops"] / (us * 1e-6) / 1e12, 2),
+                    "peak": MFMA_PEAK_TFLOPS[dtype], "unit": "TFLOP/s"}
+        else:
+            roof = {"bound": "hbm", "achieved": round(work["bytes"] / (us * 1e-6) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(work["bytes"] / (us * 1e-6) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["kernel"] = dom
+    return roof
+
+
+def run_vgg(a):
+    """cfg5: the VGG-16-shaped stack, N = 32, the most accurate candidate plan
+    per layer; a step is one pass through the thirteen convolutions (the ReLU
+    and pooling between them are not timed)."""
+    import numpy as np
+    import torch
+
+    from paper_1905_05233_amd import workloads as WL
+    from paper_1905_05233_amd.vgg import VggStack, relu_pool
+
+    dtype = a.dtype or "bf16"
+    N = 32
+    stack = VggStack(dtype)
+    x = stack.input(N)
+    stream = torch.cuda.current_stream()
+    for _ in range(a.warmup):
+        stack.forward(x)
+    torch.cuda.synchronize()
+    per_layer = np.zeros(len(stack.layers))
+    for _ in range(a.steps):
+        _, ms = stack.timed_forward(x)
+        per_layer += np.array(ms)
+    per_layer /= a.steps
+    ms_per_step = float(per_layer.sum())
+    flops = stack.direct_flops(N)
+    value = flops / (ms_per_step * 1e-3) / 1e12
+
+    # per-kernel totals over the layers, each layer's stages timed back to back
+    reps = max(5, a.steps // 5)
+    tot_us = {k: 0.0 for k in KERNEL_NAMES}
+    tot_work = {k: {"bytes": 0, "flops": 0} for k in KERNEL_NAMES}
+    xi = x
+    layers = []
+    for i, L in enumerate(stack.layers):
+        hw, C, K = L["hw"], L["C"], L["K"]
+        y = torch.empty((N, hw, hw, K), dtype=stack.tdt, device=x.device)
+        stages = make_stages(L["plan"], xi, L["w"], y, N, hw, hw, C, K, stream)
+        kus = time_kernels(stages, reps, stream)
+        wl = WL.Workload(f"vgg{i}", N=N, H=hw, W=hw, C=C, K=K, dtype=dtype, plans=(), x_dist="halfnormal")
+        work = algorithmic_work(wl, L["plan"].alpha, L["plan"].m)
+        for k in KERNEL_NAMES:
+            tot_us[k] += kus[k]
+            tot_work[k]["bytes"] += work[k]["bytes"]
+            tot_work[k]["flops"] += work[k].get("flops", 0)
+        layers.append({"layer": i, "H": hw, "C": C, "K": K, "moduli": L["spec"].moduli, "m": L["spec"].m,
+                       "alpha": L["plan"].alpha, "conv_ms": round(float(per_layer[i]), 4),
+                       "kernels_us": {k: round(v, 2) for k, v in kus.items()}})
+        xi = relu_pool(y, L["pool"])
+    dom = max(KERNEL_NAMES, key=lambda k: tot_us[k])
+    roof = roofline(dom, tot_work[dom], tot_us[dom], dtype)
+    roof["traffic"] = None
+    kernels = {k: {"total_us": round(tot_us[k], 2), "algorithmic_bytes": tot_work[k]["bytes"],
+                   "GB_s": round(tot_work[k]["bytes"] / (tot_us[k] * 1e-6) / 1e9, 1)} for k in KERNEL_NAMES}
+    kernels["contract"]["TFLOP_s"] = round(tot_work["contract"]["flops"] / (tot_us["contract"] * 1e-6) / 1e12, 2)
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s (direct-equivalent)",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+        "config": {"workload": f"VGG-16-shaped stack of 13 conv3x3 s1 p1 NHWC layers, N={N}, {dtype}, "
+                               f"most accurate candidate plan per layer (ReLU and 2x2 max-pool between "
+                               f"stages, not timed)", "N": N, "layers": layers},
+        "kernels": kernels, "roofline": roof,
+    }
+    if a.cpu_seconds > 0:
+        from oracle import conv as OC
+        from oracle import plan as OP
+        t0 = time.perf_counter()
+        done = 0
+        xs = x[:1]
+        for L in stack.layers:
+            xa = xs.float().cpu().numpy()
+            op = OP.build_plan(L["spec"].moduli, n_o=L["spec"].m, inner=L["spec"].inner)
+            OC.winograd_emulated(xa, L["w"].float().cpu().numpy(), op, dtype)
+            done += 2 * L["hw"] * L["hw"] * L["C"] * L["K"] * 9
+            xs = relu_pool(L["plan"].conv2d(xs, L["w"]), L["pool"])
+            if time.perf_counter() - t0 >= a.cpu_seconds:
+                break
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(done / dt / 1e12, 6), "unit": "TFLOP/s (direct-equivalent)",
+                               "cores": blas_threads(), "kind": "oracle",
+                               "sample": f"image 0 through the stack's layers in order, as far as {a.cpu_seconds:g} s "
+                                         f"allows, with the oracle's rounding-emulated Winograd ({dt:.1f} s)"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def blas_threads():
     try:
         from threadpoolctl import threadpool_info
@@ -84,6 +247,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="cfg2")
     ap.add_argument("--plan", type=int, default=0)
+    ap.add_argument("--dtype", default=None, choices=("f16", "bf16"),
+                    help="storage dtype of the cfg5 VGG-16 stack (default bf16)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="CPU oracle time budget (0 disables the cpu_baseline leg)")
     ap.add_argument("--graph", action="store_true", help="replay each step from a captured HIP graph")
@@ -108,6 +273,8 @@ def main(argv=None):
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     dev = torch.device("cuda:0")
+    if a.workload == "cfg5":
+        return run_vgg(a)
     wl = WL.CONFIGS[a.workload]
     ps = wl.plans[a.plan]
     tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[wl.dtype]
@@ -120,27 +287,7 @@ def main(argv=None):
     step = plan.bind_call(xd, wd, y)
     stream = torch.cuda.current_stream()
 
-    lib = NAT.lib()
-    g = plan.geometry(wl.N, wl.H, wl.W, wl.C, wl.K)
-    a2 = plan.alpha ** 2
-    U = torch.empty((a2, wl.K, g["Cp"]), dtype=tdt, device=dev)
-    V = torch.empty((a2, g["T"], g["Cp"]), dtype=tdt, device=dev)
-    M = torch.empty((a2, g["T"], g["Kp"]), dtype=torch.float32, device=dev)
-    xt = NAT.WgTensor(ctypes.c_void_p(xd.data_ptr()), wl.N, wl.H, wl.W, wl.C)
-    wt = NAT.WgTensor(ctypes.c_void_p(wd.data_ptr()), wl.K, 3, 3, wl.C)
-    yt = NAT.WgTensor(ctypes.c_void_p(y.data_ptr()), wl.N, wl.H, wl.W, wl.K)
-    sh = ctypes.c_void_p(stream.cuda_stream)
-    stages = {
-        "kernel_transform": lambda: lib.winograd_kernel_transform(plan._h, ctypes.byref(wt),
-                                                                  ctypes.c_void_p(U.data_ptr()), sh),
-        "input_transform": lambda: lib.winograd_input_transform(plan._h, ctypes.byref(xt),
-                                                                ctypes.c_void_p(V.data_ptr()), sh),
-        "contract": lambda: lib.winograd_contract(plan._h, ctypes.c_void_p(V.data_ptr()),
-                                                  ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(M.data_ptr()),
-                                                  g["T"], wl.C, wl.K, sh),
-        "output_transform": lambda: lib.winograd_output_transform(plan._h, ctypes.c_void_p(M.data_ptr()),
-                                                                  ctypes.byref(yt), sh),
-    }
+    stages = make_stages(plan, xd, wd, y, wl.N, wl.H, wl.W, wl.C, wl.K, stream)
 
     if a.profile_kernel == "copy":
         src = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device=dev).fill_(1.0)
@@ -189,22 +336,7 @@ def main(argv=None):
     # ------------------------------------------- per-kernel event timing
     # Each kernel is launched --steps times back to back on the bench stream
     # between two HIP events (its inputs are valid: every stage ran first).
-    for name in KERNEL_NAMES:
-        NAT.check(stages[name]())
-    torch.cuda.synchronize()
-    kernel_us = {}
-    for name in KERNEL_NAMES:
-        fn = stages[name]
-        for _ in range(3):
-            fn()
-        k0 = torch.cuda.Event(enable_timing=True)
-        k1 = torch.cuda.Event(enable_timing=True)
-        k0.record(stream)
-        for _ in range(a.steps):
-            fn()
-        k1.record(stream)
-        torch.cuda.synchronize()
-        kernel_us[name] = 1e3 * k0.elapsed_time(k1) / a.steps
+    kernel_us = time_kernels(stages, a.steps, stream)
 
     wtag = a.workload + (f"p{a.plan}" if a.plan else "")
     kernels = {}
@@ -217,22 +349,7 @@ def main(argv=None):
             rec["TFLOP_s"] = round(work[name]["flops"] / (us * 1e-6) / 1e12, 2)
         kernels[name] = rec
     dom = max(KERNEL_NAMES, key=lambda n: kernel_us[n])
-    us = kernel_us[dom]
-    if dom == "contract":
-        ai = work[dom]["flops"] / work[dom]["bytes"]
-        ridge = MFMA_PEAK_TFLOPS[wl.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
-        if ai >= ridge:
-            achieved = work[dom]["flops"] / (us * 1e-6) / 1e12
-            roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_PEAK_TFLOPS[wl.dtype],
-                    "unit": "TFLOP/s"}
-        else:
-            achieved = work[dom]["bytes"] / (us * 1e-6) / 1e9
-            roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    else:
-        achieved = work[dom]["bytes"] / (us * 1e-6) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["kernel"] = dom
+    roof = roofline(dom, work[dom], kernel_us[dom], wl.dtype)
     roof["traffic"] = load_traffic(dom, wtag)
 
     # --------------------------------------------- accuracy and CPU oracle
