@@ -176,9 +176,10 @@ __global__ __launch_bounds__(kThreads, 2) void contract_kernel(const unsigned ch
 // workgroups of one XCD are adjacent (the hardware hands out consecutive ids
 // round-robin across the 8 XCDs), which keeps each U[xi] in a single L2.
 //
-// The workgroup is split by role.  Wave 8, the loader, streams V tiles
-// through registers into double-buffered LDS, two tiles in flight; it issues
-// nothing but loads, so each of its waits covers exactly the tile it needs.
+// The workgroup is split by role.  The loader waves (wave 8, and wave 9 for
+// rows of up to 256 bytes) stream V tiles through registers into
+// double-buffered LDS, two or four tiles in flight; they issue nothing but
+// loads, so each of their waits covers exactly the tile they need.
 // Waves 0-7 each own 32 rows x 16 columns of the item: their U fragments stay
 // in registers while the block is unchanged (the next block is fetched one
 // item ahead), A fragments come from LDS, and the finished block of M is
@@ -187,7 +188,12 @@ __global__ __launch_bounds__(kThreads, 2) void contract_kernel(const unsigned ch
 // go through buffer descriptors whose record counts clip the ragged tails
 // (out-of-range loads return zero, out-of-range stores are dropped).
 constexpr int kStreamMmaWaves = 8;
-constexpr int kStreamThreads = (kStreamMmaWaves + 1) * 64;
+// Loader waves and the V tiles each keeps in flight (register sets), by row
+// length: short rows make short MFMA phases and need a deeper prefetch; for
+// 512-byte rows a second loader (a third wave on two SIMDs) measured slower.
+constexpr int stream_loaders(int nch) { return nch >= 8 ? 1 : 2; }
+constexpr int stream_sets(int nch) { return nch >= 8 ? 2 : 4; }
+constexpr int stream_threads(int nch) { return (kStreamMmaWaves + stream_loaders(nch)) * 64; }
 constexpr int kStreamRows = 32;
 constexpr int kStreamCols = kStreamMmaWaves * 16;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw 32-bit buffer, gfx9 family
@@ -241,7 +247,7 @@ __device__ __forceinline__ void mma16_rows2(const u32x4& x0, const u32x4& x1, co
 }
 
 template <int D, int NCH>
-__global__ __launch_bounds__(kStreamThreads, 1) void contract_stream_kernel(
+__global__ __launch_bounds__(stream_threads(NCH), 1) void contract_stream_kernel(
     const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, unsigned char* __restrict__ M,
     int64_t T, int64_t K, int rb, int64_t Kp, int num_mb, int num_nb, int64_t n_items) {
     // NCH = 16-byte chunks per lane per row: the k range of a row (rb <= 64 * NCH
@@ -275,51 +281,89 @@ __global__ __launch_bounds__(kStreamThreads, 1) void contract_stream_kernel(
         }
     };
 
-    if (wave == kStreamMmaWaves) {
-        // ------------------------------------------------------------ loader
-        constexpr int kRC = 4 * NCH;                      // 16-byte chunks per LDS row
-        constexpr int kLP = kStreamRows * kRC / 64;       // chunks per lane per tile
+    if (wave >= kStreamMmaWaves) {
+        // ----------------------------------------------------------- loaders
+        // loader lw owns every kLoaders-th 64-chunk group of a tile and keeps
+        // kSets tiles in flight in its registers
+        constexpr int kLoaders = stream_loaders(NCH);
+        constexpr int kSets = stream_sets(NCH);
+        const int lw = kLoaders == 1 ? 0 : wave - kStreamMmaWaves;
+        constexpr int kRC = 4 * NCH;                                     // 16-byte chunks per LDS row
+        constexpr int kLP = kStreamRows * kRC / (64 * kLoaders);   // chunks per lane per tile
+        static_assert(kLP * 64 * kLoaders == kStreamRows * kRC, "tile split");
         uint32_t voff[kLP];
         int lofs[kLP];
 #pragma unroll
         for (int p = 0; p < kLP; ++p) {
-            const int ci = lane + 64 * p;
+            const int ci = lw * 64 + lane + 64 * kLoaders * p;
             const int row = ci / kRC;
             const int c16 = ci % kRC;
             lofs[p] = row * kRowBytes + c16 * 16;
             voff[p] = c16 * 16 < rb ? static_cast<uint32_t>(row * rb + c16 * 16) : kOob;   // zero past the row
         }
-        u32x4 s0[kLP], s1[kLP];
         int lxi = xi, lnb = nb, lmb = mb;   // next tile to request
-        auto load = [&](u32x4 (&s)[kLP]) {
+        auto load = [&](u32x4 (&dst)[kLP]) {
             const int64_t r0 = static_cast<int64_t>(lmb) * kStreamRows;
             const auto r = make_rsrc(V + (static_cast<int64_t>(lxi) * T + r0) * rb, (T - r0) * rb);
 #pragma unroll
-            for (int p = 0; p < kLP; ++p) s[p] = __builtin_amdgcn_raw_buffer_load_b128(r, voff[p], 0, 0);
+            for (int p = 0; p < kLP; ++p) dst[p] = __builtin_amdgcn_raw_buffer_load_b128(r, voff[p], 0, 0);
             advance(lxi, lnb, lmb);
         };
-        auto park = [&](const u32x4 (&s)[kLP], int slot) {
+        auto park = [&](const u32x4 (&src)[kLP], int slot) {
 #pragma unroll
-            for (int p = 0; p < kLP; ++p) *reinterpret_cast<u32x4*>(abuf + slot * kABytes + lofs[p]) = s[p];
+            for (int p = 0; p < kLP; ++p) *reinterpret_cast<u32x4*>(abuf + slot * kABytes + lofs[p]) = src[p];
         };
-        load(s0);
-        if (n_mine > 1) load(s1);
-        park(s0, 0);
-        if (n_mine > 2) load(s0);
-        __syncthreads();
-        // during item i: park tile i+1, request tile i+3 in its registers
-        for (int i = 0; i < n_mine; i += 2) {
-            if (i + 1 < n_mine) {
-                park(s1, 1);
-                if (i + 3 < n_mine) load(s1);
-            }
+        if constexpr (kSets == 2) {
+            // two register sets, written out (the generic loop below costs
+            // registers that the 512-byte rows do not have to spare)
+            u32x4 s0[kLP], s1[kLP];
+            load(s0);
+            if (n_mine > 1) load(s1);
+            park(s0, 0);
+            if (n_mine > 2) load(s0);
             __syncthreads();
-            if (i + 1 >= n_mine) break;
-            if (i + 2 < n_mine) {
-                park(s0, 0);
-                if (i + 4 < n_mine) load(s0);
+            // during item i: park tile i+1, request tile i+3 in its registers
+            for (int i = 0; i < n_mine; i += 2) {
+                if (i + 1 < n_mine) {
+                    park(s1, 1);
+                    if (i + 3 < n_mine) load(s1);
+                }
+                __syncthreads();
+                if (i + 1 >= n_mine) break;
+                if (i + 2 < n_mine) {
+                    park(s0, 0);
+                    if (i + 4 < n_mine) load(s0);
+                }
+                __syncthreads();
             }
+        } else {
+            u32x4 s[kSets][kLP];
+            // tiles 0 .. kSets-1 requested, tile 0 parked, its registers refilled
+#pragma unroll
+            for (int j = 0; j < kSets; ++j)
+                if (j < n_mine) load(s[j]);
+            park(s[0], 0);
+            if (kSets < n_mine) load(s[0]);
             __syncthreads();
+            // during item i: park tile i+1 into LDS slot (i+1) mod 2, request tile
+            // i+1+kSets in its registers (the loop is unrolled so that the register
+            // set is a compile-time index)
+            for (int i = 0; i < n_mine; i += kSets) {
+                bool done = false;
+#pragma unroll
+                for (int j = 0; j < kSets; ++j) {
+                    if (!done) {
+                        const int ii = i + j;
+                        if (ii + 1 < n_mine) {
+                            park(s[(j + 1) % kSets], (ii + 1) & 1);
+                            if (ii + 1 + kSets < n_mine) load(s[(j + 1) % kSets]);
+                        }
+                        __syncthreads();
+                        done = ii + 1 >= n_mine;
+                    }
+                }
+                if (done) break;
+            }
         }
         return;
     }
@@ -414,7 +458,7 @@ hipError_t launch_stream(const Geometry& g, const void* V, const void* U, float*
     const int num_nb = static_cast<int>((g.K + kStreamCols - 1) / kStreamCols);
     const int64_t n_items = static_cast<int64_t>(num_mb) * num_nb * g.alpha * g.alpha;
     const int64_t grid = std::min<int64_t>(n_items, device_cu_count());
-    hipLaunchKernelGGL((contract_stream_kernel<D, NCH>), dim3(static_cast<unsigned>(grid)), dim3(kStreamThreads), 0,
+    hipLaunchKernelGGL((contract_stream_kernel<D, NCH>), dim3(static_cast<unsigned>(grid)), dim3(stream_threads(NCH)), 0,
                        stream, static_cast<const unsigned char*>(V), static_cast<const unsigned char*>(U),
                        reinterpret_cast<unsigned char*>(M), g.T, g.K, static_cast<int>(row_bytes), g.Kp, num_mb,
                        num_nb, n_items);
