@@ -105,6 +105,24 @@ wg_status winograd_plan_create(const wg_poly_set* set, int m, int r, wg_dtype dt
 wg_status winograd_plan_create_str(const char* moduli, const char* inner, int m, int r,
                                    wg_dtype dtype, wg_plan* out);
 
+/* Where the CRT factors N_i of eq. (1) go.  WG_FACTORS_IN_B is the paper's
+ * construction (Section 2.2: the matrices G and A are not scaled by N_i, the
+ * factors sit in B through E).  WG_FACTORS_IN_G multiplies the kernel
+ * residues by N_i instead: G' = [vec(R_m[N_i a^k])] (for a linear modulus
+ * a - p the row [p^0 .. p^(r-1)] times the constant N_i = 1 / M_i(p)) and
+ * E_i = [vec(R_M[a^k M_i])].  Both are exact; they round differently.  For
+ * linear points the second gives the matrices of Lavin & Gray's F(4,3). */
+typedef enum { WG_FACTORS_IN_B = 0, WG_FACTORS_IN_G = 1 } wg_crt_factors;
+
+typedef struct {
+    wg_crt_factors factors;
+} wg_plan_options;
+
+/* winograd_plan_create_str with options (opts == NULL means all defaults:
+ * WG_FACTORS_IN_B).  An unknown option value is WG_ERR_ARG. */
+wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, int r, wg_dtype dtype,
+                                  const wg_plan_options* opts, wg_plan* out);
+
 /* Release a plan (NULL is ignored).  Does not free a bound workspace. */
 void winograd_plan_destroy(wg_plan plan);
 

@@ -39,6 +39,14 @@ notes of the repository):
   inner-point order, the pseudo-point last.
 * Moduli are made monic; they must be irreducible and pairwise coprime
   (Section 2.1).
+
+Option (an accuracy variant the paper names as complementary, Section 5):
+``factors="G"`` moves each CRT factor N_i from the input side to the kernel
+side.  Eq. (1) multiplies the residue product s_i = (g d) mod m_i by N_i; since
+(N_i g mod m_i)(d mod m_i) = N_i g d (mod m_i), the factor may multiply the
+kernel residue instead: G' gets the columns vec(R_m[N_i a^k]) (for a linear
+modulus the row [p^0 .. p^(r-1)] times the scalar N_i(p)) and E the columns
+vec(R_M[a^k M_i]).  The exact algorithm is unchanged; the rounding is not.
 """
 from dataclasses import dataclass, field
 from fractions import Fraction
@@ -234,15 +242,22 @@ class ExactPlan:
         return [list(r) for r in zip(*self.B)]
 
 
-def residue_map(m, ncols):
-    """[vec(R_m[a^0]) ... vec(R_m[a^(ncols-1)])]: deg(m) x ncols (Algorithm 1)."""
+def residue_map(m, ncols, factor=None):
+    """[vec(R_m[f a^0]) ... vec(R_m[f a^(ncols-1)])]: deg(m) x ncols
+    (Algorithm 1's G' and A' with f = 1; f = N_i moves the CRT factor)."""
     d = P.deg(m)
-    cols = [P.vec(P.rem(P.power_of_a(k), m), d) for k in range(ncols)]
+    f = P.ONE if factor is None else factor
+    cols = [P.vec(P.rem(P.mul(f, P.power_of_a(k)), m), d) for k in range(ncols)]
     return [[cols[j][i] for j in range(ncols)] for i in range(d)]
 
 
-def build_plan(moduli_spec, n_o, n_h=3, inner="0,-1,inf"):
-    """Build G^W, A^W, B^W exactly for F(n_o, n_h) from a modulus set."""
+def build_plan(moduli_spec, n_o, n_h=3, inner="0,-1,inf", factors="B"):
+    """Build G^W, A^W, B^W exactly for F(n_o, n_h) from a modulus set.
+
+    ``factors`` places the CRT factors N_i: "B" (the paper's matrices, inside
+    E) or "G" (multiplying the kernel residues)."""
+    if factors not in ("B", "G"):
+        raise ValueError("factors must be 'B' or 'G'")
     finite, has_inf = parse_modulus_set(moduli_spec)
     inner_pts, inner_inf = parse_points(inner)
     n = n_h + n_o - 2
@@ -266,18 +281,25 @@ def build_plan(moduli_spec, n_o, n_h=3, inner="0,-1,inf"):
     plan = ExactPlan(n_o=n_o, n_h=n_h, moduli=finite, has_inf=has_inf,
                      inner_points=inner_pts, inner_inf=inner_inf)
 
+    # CRT factors of eq. (1): M = prod m_i, M_i = M / m_i, N_i M_i = 1 mod m_i
+    Mpoly = P.product(finite)
+    Mi = [P.exact_div(Mpoly, m) for m in finite]
+    N = [P.inverse_mod(Mi_, m) for m, Mi_ in zip(finite, Mi)]
+
     # ---- Algorithm 1: G^W and A^W -----------------------------------------
     G, A, blocks = [], [], []
-    for m in finite:
+    for m, Ni in zip(finite, N):
         d = P.deg(m)
         blk = {"m": m, "d": d}
+        kf = Ni if factors == "G" else None
         if d == 1:
             p = -m[0]                      # root of the monic a - p
-            Gi = [[p ** k for k in range(n_h)]]
+            s_ = Ni[0] if factors == "G" else Fraction(1)   # N_i is the constant 1 / M_i(p)
+            Gi = [[s_ * p ** k for k in range(n_h)]]
             Ai = [[p ** k for k in range(n_o)]]
         else:
             tc = inner_toom_cook(d, inner_pts, inner_inf)
-            Gp = residue_map(m, n_h)      # G'
+            Gp = residue_map(m, n_h, kf)  # G'
             Ap = residue_map(m, n_o)      # A'
             Gi = _matmul(tc.G, Gp)
             Ai = _matmul(tc.A, Ap)
@@ -291,8 +313,6 @@ def build_plan(moduli_spec, n_o, n_h=3, inner="0,-1,inf"):
         A.append([Fraction(0)] * (n_o - 1) + [Fraction(1)])
 
     # ---- Algorithm 2: B^W = [E C | vec(M)] -------------------------------
-    Mpoly = P.product(finite)
-    Mi = [P.exact_div(Mpoly, m) for m in finite]
     # block-diagonal C
     Cblocks = []
     for blk in blocks:
@@ -319,14 +339,14 @@ def build_plan(moduli_spec, n_o, n_h=3, inner="0,-1,inf"):
                 C[r0 + i][c0 + j] = v
         r0 += len(b)
         c0 += len(b[0])
-    # E: columns vec(R_M[a^k N_i M_i]), k < d, padded to n + 1 rows
-    Ecols, N = [], []
-    for m, Mi_ in zip(finite, Mi):
-        Ni = P.inverse_mod(Mi_, m)
-        N.append(Ni)
+    # E: columns vec(R_M[a^k N_i M_i]) (vec(R_M[a^k M_i]) with the factors in G), k < d,
+    # padded to n + 1 rows
+    Ecols = []
+    for bi, (m, Mi_, Ni) in enumerate(zip(finite, Mi, N)):
+        f = Mi_ if factors == "G" else P.mul(Ni, Mi_)
         for k in range(P.deg(m)):
-            Ecols.append(P.vec(P.rem(P.mul(P.power_of_a(k), P.mul(Ni, Mi_)), Mpoly), n + 1))
-        blocks[len(N) - 1]["E"] = Ecols[-P.deg(m):]
+            Ecols.append(P.vec(P.rem(P.mul(P.power_of_a(k), f), Mpoly), n + 1))
+        blocks[bi]["E"] = Ecols[-P.deg(m):]
     E = [[Ecols[j][i] for j in range(len(Ecols))] for i in range(n + 1)]
     EC = _matmul(E, C)
     if has_inf:

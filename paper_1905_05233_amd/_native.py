@@ -26,6 +26,13 @@ class WgPolySet(ctypes.Structure):
                 ("inner_pts", ctypes.POINTER(WgRational)), ("inner_inf", ctypes.c_int)]
 
 
+class WgPlanOptions(ctypes.Structure):
+    _fields_ = [("factors", ctypes.c_int)]
+
+
+FACTOR_CODES = {"B": 0, "G": 1}
+
+
 class WgTensor(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("n", ctypes.c_int64), ("h", ctypes.c_int64),
                 ("w", ctypes.c_int64), ("c", ctypes.c_int64)]
@@ -58,6 +65,8 @@ def lib():
                                                 ctypes.c_int, plan_p]),
         "winograd_plan_create_str": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_char_p, ctypes.c_int, ctypes.c_int,
                                                     ctypes.c_int, plan_p]),
+        "winograd_plan_create_ex": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_char_p, ctypes.c_int, ctypes.c_int,
+                                                   ctypes.c_int, ctypes.POINTER(WgPlanOptions), plan_p]),
         "winograd_plan_destroy": (None, [P]),
         "winograd_plan_alpha": (ctypes.c_int, [P]),
         "winograd_plan_info": (ctypes.c_int, [P] + [ctypes.POINTER(ctypes.c_int)] * 5),

@@ -216,6 +216,24 @@ wg_status winograd_plan_create_str(const char* moduli, const char* inner, int m,
     });
 }
 
+wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, int r, wg_dtype dtype,
+                                  const wg_plan_options* opts, wg_plan* out) {
+    return guarded([&]() -> wg_status {
+        wg_status s = check_create_args(m, r, dtype, out);
+        if (s != WG_OK) return s;
+        if (!moduli) return fail(WG_ERR_ARG, "null modulus string");
+        const int factors = opts ? static_cast<int>(opts->factors) : WG_FACTORS_IN_B;
+        if (factors != WG_FACTORS_IN_B && factors != WG_FACTORS_IN_G)
+            return fail(WG_ERR_ARG, "unknown CRT factor placement");
+        const std::vector<wg::Modulus> mods = wg::parse_moduli(moduli);
+        std::vector<wg::Rat> pts;
+        bool inf = true;
+        if (inner && inner[0] != '\0') wg::parse_points(inner, &pts, &inf);
+        else pts = {wg::Rat(0), wg::Rat(-1)};
+        return finish_plan(wg::build_transforms(mods, pts, inf, m, r, factors == WG_FACTORS_IN_G), dtype, out);
+    });
+}
+
 void winograd_plan_destroy(wg_plan plan) { delete plan; }
 
 int winograd_plan_alpha(wg_plan plan) { return plan ? plan->tr.alpha : 0; }

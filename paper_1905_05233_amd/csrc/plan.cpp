@@ -23,6 +23,10 @@
 //     row and B^W = E C (Table 1's all-quadratic columns);
 //   - Winograd-domain rows: modulus order, 2d-1 rows per degree-d modulus
 //     in inner-point order, infinity last.
+// Option: the CRT factors N_i may instead multiply the kernel residues
+// ((N_i g mod m_i)(d mod m_i) = N_i g d mod m_i), giving G' = [vec(R_m[N_i
+// a^k])] and E_i = [vec(R_M[a^k M_i])]: the same exact algorithm with other
+// roundings (an accuracy variant of the kind Section 5 names as complementary).
 #include "plan.hpp"
 
 #include <algorithm>
@@ -170,11 +174,13 @@ Mat matmul(const Mat& X, const Mat& Y) {
 }
 
 // d x ncols matrix whose column k is vec(R_m[a^k])  (G' / A' of Algorithm 1).
-Mat residue_columns(const Poly& mod, int ncols) {
+// [vec(R_mod[f a^0]) .. vec(R_mod[f a^(ncols-1)])]: Algorithm 1's G' and A'
+// with f = 1; f = N_i carries the CRT factor on the kernel side.
+Mat residue_columns(const Poly& mod, int ncols, const Poly& f = Poly::constant(Rat(1))) {
     const int d = mod.deg();
     Mat R(static_cast<size_t>(d), std::vector<Rat>(static_cast<size_t>(ncols)));
     for (int k = 0; k < ncols; ++k) {
-        const std::vector<Rat> v = Poly::monomial(k).rem(mod).vec(d);
+        const std::vector<Rat> v = (f * Poly::monomial(k)).rem(mod).vec(d);
         for (int i = 0; i < d; ++i) R[static_cast<size_t>(i)][static_cast<size_t>(k)] = v[static_cast<size_t>(i)];
     }
     return R;
@@ -260,7 +266,7 @@ void parse_points(const std::string& text, std::vector<Rat>* pts, bool* with_inf
 }
 
 Transforms build_transforms(const std::vector<Modulus>& moduli_in, const std::vector<Rat>& inner_pts,
-                            bool inner_inf, int m, int r) {
+                            bool inner_inf, int m, int r, bool factors_in_g) {
     if (m < 1 || r < 1) throw PlanError(kErrArg, "tile sizes must be positive");
     const int n = m + r - 2;  // degree of the product polynomial s(a)
     std::vector<Poly> mods;
@@ -289,18 +295,31 @@ Transforms build_transforms(const std::vector<Modulus>& moduli_in, const std::ve
             if (poly_gcd(mods[i], mods[j], nullptr).deg() != 0)
                 throw PlanError(kErrNotCoprime, "moduli are not pairwise coprime");
 
+    // eq. (1): M = prod m_i, M_i = M / m_i, N_i M_i = 1 (mod m_i)
+    Poly M = Poly::constant(Rat(1));
+    for (const Poly& p : mods) M = M * p;
+    std::vector<Poly> Mis, Nis;
+    for (const Poly& mi : mods) {
+        Mis.push_back(M.exact_div(mi));
+        Nis.push_back(inverse_mod(Mis.back(), mi));
+    }
+
     // ---- Algorithm 1 -------------------------------------------------------
+    // factors_in_g: the kernel residues carry N_i (rows scaled by the constant
+    // N_i(p) for a linear modulus, G' = [vec(R_m[N_i a^k])] otherwise)
     Mat G, A;
     std::vector<InnerTC> tcs(mods.size());
     for (size_t i = 0; i < mods.size(); ++i) {
         const Poly& mi = mods[i];
         const int d = mi.deg();
+        const Poly kf = factors_in_g ? Nis[i] : Poly::constant(Rat(1));
         if (d == 1) {
             const Rat p = -mi.coef(0);
+            const Rat sc = kf.coef(0);   // N_i is the constant 1 / M_i(p)
             std::vector<Rat> g, a;
             Rat pw(1);
             for (int k = 0; k < std::max(r, m); ++k) {
-                if (k < r) g.push_back(pw);
+                if (k < r) g.push_back(sc * pw);
                 if (k < m) a.push_back(pw);
                 pw = pw * p;
             }
@@ -308,7 +327,7 @@ Transforms build_transforms(const std::vector<Modulus>& moduli_in, const std::ve
             A.push_back(a);
         } else {
             tcs[i] = inner_toom_cook(d, inner_pts, inner_inf);
-            const Mat Gi = matmul(tcs[i].G, residue_columns(mi, r));
+            const Mat Gi = matmul(tcs[i].G, residue_columns(mi, r, kf));
             const Mat Ai = matmul(tcs[i].A, residue_columns(mi, m));
             G.insert(G.end(), Gi.begin(), Gi.end());
             A.insert(A.end(), Ai.begin(), Ai.end());
@@ -324,8 +343,6 @@ Transforms build_transforms(const std::vector<Modulus>& moduli_in, const std::ve
     const int alpha = static_cast<int>(G.size());
 
     // ---- Algorithm 2 -------------------------------------------------------
-    Poly M = Poly::constant(Rat(1));
-    for (const Poly& p : mods) M = M * p;
     const int rowsB = n + 1;
     // E C computed block by block: for modulus i, E_i (rowsB x d) times C_i
     // (d x (2d-1)) fills the columns of that modulus' domain rows.
@@ -334,9 +351,8 @@ Transforms build_transforms(const std::vector<Modulus>& moduli_in, const std::ve
     for (size_t i = 0; i < mods.size(); ++i) {
         const Poly& mi = mods[i];
         const int d = mi.deg();
-        const Poly Mi = M.exact_div(mi);
-        const Poly Ni = inverse_mod(Mi, mi);
-        const Poly NiMi = Ni * Mi;
+        // E_i = [vec(R_M[a^k N_i M_i])], or [vec(R_M[a^k M_i])] with the factors in G
+        const Poly NiMi = factors_in_g ? Mis[i] : Nis[i] * Mis[i];
         Mat Ei(static_cast<size_t>(rowsB), std::vector<Rat>(static_cast<size_t>(d)));
         for (int k = 0; k < d; ++k) {
             const std::vector<Rat> v = (Poly::monomial(k) * NiMi).rem(M).vec(rowsB);

@@ -37,14 +37,24 @@ def _tensor(t, name, shape=None):
 class Plan:
     """A Winograd plan F(m x m, 3 x 3) built from a modulus set (Algorithms 1, 2)."""
 
-    def __init__(self, moduli, m, dtype="f32", inner="0,-1,inf", r=3):
+    def __init__(self, moduli, m, dtype="f32", inner="0,-1,inf", r=3, factors="B"):
+        """``factors``: where the CRT factors N_i go, "B" (the paper's
+        matrices) or "G" (on the kernel residues)."""
         if dtype not in N.DTYPE_CODES:
             raise ValueError(f"dtype must be one of {list(N.DTYPE_CODES)}")
+        if factors not in N.FACTOR_CODES:
+            raise ValueError(f"factors must be one of {list(N.FACTOR_CODES)}")
         self._lib = N.lib()
         self._h = ctypes.c_void_p()
-        N.check(self._lib.winograd_plan_create_str(moduli.encode(), (inner or "").encode(), int(m), int(r),
-                                                   N.DTYPE_CODES[dtype], ctypes.byref(self._h)))
-        self.moduli, self.inner, self.dtype = moduli, inner, dtype
+        if factors == "B":
+            N.check(self._lib.winograd_plan_create_str(moduli.encode(), (inner or "").encode(), int(m), int(r),
+                                                       N.DTYPE_CODES[dtype], ctypes.byref(self._h)))
+        else:
+            opts = N.WgPlanOptions(N.FACTOR_CODES[factors])
+            N.check(self._lib.winograd_plan_create_ex(moduli.encode(), (inner or "").encode(), int(m), int(r),
+                                                      N.DTYPE_CODES[dtype], ctypes.byref(opts),
+                                                      ctypes.byref(self._h)))
+        self.moduli, self.inner, self.dtype, self.factors = moduli, inner, dtype, factors
         vals = [ctypes.c_int() for _ in range(5)]
         N.check(self._lib.winograd_plan_info(self._h, *[ctypes.byref(v) for v in vals]))
         self.m, self.r, self.alpha, self.tile_in, _ = [v.value for v in vals]
@@ -74,7 +84,7 @@ class Plan:
         self._h = ctypes.c_void_p()
         N.check(self._lib.winograd_plan_create(ctypes.byref(ps), int(m), int(r), N.DTYPE_CODES[dtype],
                                                ctypes.byref(self._h)))
-        self.moduli, self.inner, self.dtype = moduli, inner_points, dtype
+        self.moduli, self.inner, self.dtype, self.factors = moduli, inner_points, dtype, "B"
         vals = [ctypes.c_int() for _ in range(5)]
         N.check(self._lib.winograd_plan_info(self._h, *[ctypes.byref(v) for v in vals]))
         self.m, self.r, self.alpha, self.tile_in, _ = [v.value for v in vals]

@@ -61,6 +61,38 @@ def test_plan_exact_parity_with_oracle(spec, m, inner):
         assert np.array_equal(ours.view(np.uint32), want.view(np.uint32)), which
 
 
+@pytest.mark.parametrize("spec,m,inner", PLAN_SETS[::2])
+def test_factors_in_g_plan_parity_with_oracle(spec, m, inner):
+    """winograd_plan_create_ex with WG_FACTORS_IN_G: exact matrices and fp32
+    tables equal the oracle's factors="G" construction."""
+    ref = OP.build_plan(spec, n_o=m, inner=inner, factors="G")
+    p = Plan(spec, m=m, dtype="f32", inner=inner, factors="G")
+    for which, mat in (("G", ref.G), ("A", ref.A), ("B", ref.B)):
+        assert p.matrix(which) == mat
+        ours = np.array(p.matrix_f32(which), dtype=np.float32)
+        want = np.array([[OF.fraction_to_f32(v) for v in row] for row in mat], dtype=np.float32)
+        assert np.array_equal(ours.view(np.uint32), want.view(np.uint32)), which
+
+
+def test_create_ex_defaults_and_errors():
+    lib = N.lib()
+    h = ctypes.c_void_p()
+    # NULL options = the paper's placement
+    assert lib.winograd_plan_create_ex(WL.F4_LINEAR.encode(), b"", 4, 3, 0, None, ctypes.byref(h)) == 0
+    p = Plan(WL.F4_LINEAR, m=4)
+    buf = (N.WgRational * (p.alpha * 3))()
+    assert lib.winograd_plan_matrix(h, b"G", buf, len(buf)) == 0
+    assert [[Fraction(buf[i * 3 + j].num, buf[i * 3 + j].den) for j in range(3)] for i in range(p.alpha)] == \
+        p.matrix("G")
+    lib.winograd_plan_destroy(h)
+    bad = N.WgPlanOptions(7)
+    h2 = ctypes.c_void_p()
+    assert lib.winograd_plan_create_ex(WL.F4_LINEAR.encode(), b"", 4, 3, 0, ctypes.byref(bad), ctypes.byref(h2)) == 1
+    assert not h2.value
+    with pytest.raises(ValueError):
+        Plan(WL.F4_LINEAR, m=4, factors="A")
+
+
 def test_struct_entry_matches_string_entry():
     p1 = Plan(WL.F6_TWO_QUAD, m=6, dtype="bf16")
     mods = [[0, 1], [1, 1], [-1, 1], [1, 0, 1], [-2, 0, 1], None]

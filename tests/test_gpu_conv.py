@@ -105,3 +105,37 @@ def test_workspace_reuse_and_external_binding():
     assert torch.equal(y1, y2)
     ref = OC.direct_f64(xs, ws_)
     assert OC.rel_l2(to_np(y_small), ref) < 1e-5
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("spec,m", [(WL.F2_LINEAR, 2), (WL.F4_LINEAR, 4), (WL.F4_A2P1, 4), (WL.F6_TWO_QUAD, 6)])
+def test_factors_in_g_parity(spec, m, dtype):
+    """Plans with the CRT factors on the kernel side: the 2x rule and the
+    element-wise bound against the oracle's emulation of the same plan."""
+    from paper_1905_05233_amd.winograd import Plan
+    N, H, W, C, K = 2, 26, 30, 24, 40
+    x, w = WL.draw_inputs(N, H, W, C, K, "halfnormal", seed=5 * m)
+    x, w = OF.to_dtype(x, dtype), OF.to_dtype(w, dtype)
+    op = OP.build_plan(spec, n_o=m, factors="G")
+    yg = to_np(Plan(spec, m=m, dtype=dtype, factors="G").conv2d(to_dev(x, dtype), to_dev(w, dtype)))
+    y64 = OC.direct_f64(x, w)
+    yo = OC.winograd_emulated(x, w, op, dtype)
+    err_gpu, err_or = OC.rel_l2(yg, y64), OC.rel_l2(yo, y64)
+    err_b = OC.rel_l2(OC.winograd_emulated(x, w, OP.build_plan(spec, n_o=m), dtype), y64)
+    print(f"[factors-G] {spec} {dtype}: gpu {err_gpu:.3e} oracle {err_or:.3e} (factors in B: {err_b:.3e})",
+          flush=True)
+    assert err_gpu <= 2 * err_or
+    bound = elementwise_bound(x, w, op, dtype, y64)
+    assert np.all(np.abs(yg.astype(np.float64) - yo) <= 2 * bound)
+
+
+def test_factors_in_g_bit_exact_dyadic():
+    """F(2,3) with the factors in G has entries 0, +-1, +-1/2: on small
+    integers every rounding is exact and the result is direct convolution."""
+    from paper_1905_05233_amd.winograd import Plan
+    x, w = WL.draw_inputs(2, 9, 13, 5, 7, "int2", seed=21)
+    op = OP.build_plan(WL.F2_LINEAR, n_o=2, factors="G")
+    ref = OC.direct_f64(x, w)
+    assert np.array_equal(OC.winograd_emulated(x, w, op, "f32").astype(np.float64), ref)
+    y = to_np(Plan(WL.F2_LINEAR, m=2, dtype="f32", factors="G").conv2d(to_dev(x, "f32"), to_dev(w, "f32")))
+    assert np.array_equal(y.astype(np.float64), ref)

@@ -65,6 +65,14 @@ def test_exact_winograd_equals_direct(spec, m):
         assert OC.winograd_exact(x, w, pl) == OC.direct_exact(x, w)
 
 
+@pytest.mark.parametrize("spec,m", ALL_SETS)
+def test_exact_winograd_equals_direct_with_factors_in_g(spec, m):
+    """The CRT factors on the kernel side give the same exact convolution."""
+    pl = OP.build_plan(spec, n_o=m, factors="G")
+    x, w = _frac_inputs(1, 2 * m - 1, m + 1, 2, 2, seed=3 * m)
+    assert OC.winograd_exact(x, w, pl) == OC.direct_exact(x, w)
+
+
 def test_exact_winograd_worked_example_plan():
     for b, c in [(0, 1), (1, 1), (0, -2)]:
         pl = OP.build_plan(["0", (Fraction(c), Fraction(b), Fraction(1)), "inf"], n_o=2, inner="0,1,inf")

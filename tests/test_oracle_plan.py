@@ -223,3 +223,63 @@ def test_polynomial_helpers_against_brute_force():
     assert P.rem(P.mul(inv, P.parse("a+2")), m) == P.ONE
     assert P.parse("a^2-a+1") == P.poly([1, -1, 1])
     assert P.parse("2a^3-1/2") == P.poly([Fraction(-1, 2), 0, 0, 2])
+
+
+# ---------------------------------------------------------------------------
+# CRT factors on the kernel side (factors="G")
+# ---------------------------------------------------------------------------
+
+def test_factors_in_g_reproduce_lavin_f43_exactly():
+    """With the CRT factors N_i moved onto the kernel residues, the points
+    {0, 1, -1, 2, -2, inf} give exactly the F(4,3) matrices Lavin & Gray
+    published: G (with its 1/4, -1/6, 1/24 ... rows), B^T and A^T."""
+    gold = load_golden("lavin_gray_2016.json")["F(4,3)"]
+    pl = OP.build_plan(gold["points"], n_o=4, factors="G")
+    assert pl.G == frac_matrix(gold["G"])
+    assert pl.BT == frac_matrix(gold["BT"])
+    assert [list(r) for r in zip(*pl.A)] == frac_matrix(gold["AT"])
+
+
+def test_factors_in_g_reproduce_lavin_f23_up_to_row_signs():
+    """F(2,3) on {0, 1, -1, inf}: Lavin & Gray's matrices up to the signs of
+    single domain rows (G and B^T entries equal in magnitude, and each row's
+    rank-1 term A (x) G (x) B^T is the published one)."""
+    gold = load_golden("lavin_gray_2016.json")["F(2,3)"]
+    pl = OP.build_plan(gold["points"], n_o=2, factors="G")
+    G, BT, AT = frac_matrix(gold["G"]), frac_matrix(gold["BT"]), frac_matrix(gold["AT"])
+    assert [[abs(v) for v in r] for r in pl.G] == [[abs(v) for v in r] for r in G]
+    assert [[abs(v) for v in r] for r in pl.BT] == [[abs(v) for v in r] for r in BT]
+    A = [list(r) for r in zip(*AT)]
+    assert _triples(pl.G, pl.A, pl.BT) == _triples(G, A, BT)
+
+
+@pytest.mark.parametrize("spec,m,inner", [
+    ("0,1,-1,1/2,-1/2,inf", 4, "0,-1,inf"), ("0,1,-1,a^2+1,inf", 4, "0,-1,inf"),
+    ("0,-1,1,a^2+1,a^2-2,inf", 6, "0,-1,inf"), ("a^2+1,a^2+2", 2, "0,-1,inf"),
+    ("0,-1,a^3+2,inf", 4, "0,-1,1,-2,inf"), ("0,a^2+a+1,inf", 2, "0,1,inf"),
+])
+def test_factors_in_g_move_exactly_the_crt_factors(spec, m, inner):
+    """eq. (1): moving N_i from B to G leaves the reconstruction identity and
+    A unchanged; a linear modulus's G row is multiplied, and its B column
+    divided, by the constant N_i = 1 / M_i(p); a degree-d block's kernel
+    residues are multiplied by N_i mod m_i."""
+    pb = OP.build_plan(spec, n_o=m, inner=inner)
+    pg = OP.build_plan(spec, n_o=m, inner=inner, factors="G")
+    assert OP.trilinear_defect(pg) == 0
+    assert pg.A == pb.A and pg.alpha == pb.alpha
+    x = 0
+    for blk, Ni, Mi in zip(pb.blocks, pb.N, pb.Mi):
+        d = blk["d"]
+        rows = 1 if d == 1 else 2 * d - 1
+        if d == 1:
+            c = Ni[0]
+            p_ = -blk["m"][0]
+            assert c * P.evaluate(Mi, p_) == 1
+            assert pg.G[x] == [c * v for v in pb.G[x]]
+            assert [r[x] for r in pg.B] == [v / c for v in (r[x] for r in pb.B)]
+        else:
+            Gp = OP.residue_map(blk["m"], 3, Ni)
+            want = [[sum((blk["tc"].G[i][k] * Gp[k][j] for k in range(d)), Fraction(0)) for j in range(3)]
+                    for i in range(rows)]
+            assert pg.G[x:x + rows] == want
+        x += rows
