@@ -3,8 +3,9 @@
 
 One step = one full layer through eq. (2) of Barabasz & Gregg (arXiv
 1905.05233): kernel transform, input transform, alpha'^2 batched matrix-core
-contraction and output transform, on seeded synthetic inputs already resident
-in HBM.  Default workload: conv3x3 stride 1 pad 1, N=8, C=K=128, H=W=56, fp32,
+contraction and output transform (separate kernels, or the last two fused
+into one where the library picks that path for the layer shape), on seeded
+synthetic inputs already resident in HBM.  Default workload: conv3x3 stride 1 pad 1, N=8, C=K=128, H=W=56, fp32,
 F(4x4,3x3) with points {0, 1, -1, 1/2, -1/2, inf}.
 
 Prints one JSON line: direct-equivalent TFLOP/s (2 N H W C K 9 flops per
@@ -33,9 +34,10 @@ if ROOT not in sys.path:
 METRIC = "direct-equiv conv TFLOP/s + MFMA util/HBM GB/s; rel-L2 err vs fp64 direct"
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0, "bf16": 2500.0}
-KERNEL_NAMES = ("kernel_transform", "input_transform", "contract", "output_transform")
+KERNEL_NAMES = ("kernel_transform", "input_transform", "contract", "output_transform", "contract_output")
 KERNEL_SOURCES = {"kernel_transform": "transforms.hip", "input_transform": "transforms.hip",
-                  "contract": "contract.hip", "output_transform": "transforms.hip"}
+                  "contract": "contract.hip", "output_transform": "transforms.hip",
+                  "contract_output": "fused.hip"}
 
 
 def algorithmic_work(wl, alpha, m):
@@ -50,6 +52,9 @@ def algorithmic_work(wl, alpha, m):
         "input_transform": {"bytes": wl.N * wl.H * wl.W * C * s + a2 * T * C * s},
         "contract": {"flops": 2 * a2 * T * C * K, "bytes": a2 * (T * C * s + K * C * s + T * K * 4)},
         "output_transform": {"bytes": a2 * T * K * 4 + wl.N * wl.H * wl.W * K * s},
+        # fused: V and U in, y out, no M
+        "contract_output": {"flops": 2 * a2 * T * C * K,
+                            "bytes": a2 * (T * C * s + K * C * s) + wl.N * wl.H * wl.W * K * s},
         "T": T,
     }
 
@@ -73,33 +78,40 @@ def load_traffic(kernel, workload_tag):
 
 
 def make_stages(plan, xd, wd, y, N_, H, W, C, K, stream):
-    """Launchers of the four stage kernels of one layer (intermediates
-    allocated here), each returning the library's status."""
+    """Launchers of the stage kernels that conv2d runs for this layer (the
+    path the plan takes for the shape; intermediates allocated here), in
+    launch order, each returning the library's status."""
     import torch
     from paper_1905_05233_amd import _native as NAT
     lib = NAT.lib()
     g = plan.geometry(N_, H, W, C, K)
     a2 = plan.alpha ** 2
     dev = xd.device
+    fused = plan.conv_path(N_, H, W, C, K) == "fused"
     U = torch.empty((a2, K, g["Cp"]), dtype=xd.dtype, device=dev)
     V = torch.empty((a2, g["T"], g["Cp"]), dtype=xd.dtype, device=dev)
-    M = torch.empty((a2, g["T"], g["Kp"]), dtype=torch.float32, device=dev)
+    M = None if fused else torch.empty((a2, g["T"], g["Kp"]), dtype=torch.float32, device=dev)
     xt = NAT.WgTensor(ctypes.c_void_p(xd.data_ptr()), N_, H, W, C)
     wt = NAT.WgTensor(ctypes.c_void_p(wd.data_ptr()), K, 3, 3, C)
     yt = NAT.WgTensor(ctypes.c_void_p(y.data_ptr()), N_, H, W, K)
     sh = ctypes.c_void_p(stream.cuda_stream)
     # the closures keep U, V, M and the tensor descriptors alive
-    return {
+    stages = {
         "kernel_transform": lambda: lib.winograd_kernel_transform(plan._h, ctypes.byref(wt),
                                                                   ctypes.c_void_p(U.data_ptr()), sh),
         "input_transform": lambda: lib.winograd_input_transform(plan._h, ctypes.byref(xt),
                                                                 ctypes.c_void_p(V.data_ptr()), sh),
-        "contract": lambda: lib.winograd_contract(plan._h, ctypes.c_void_p(V.data_ptr()),
-                                                  ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(M.data_ptr()),
-                                                  g["T"], C, K, sh),
-        "output_transform": lambda: lib.winograd_output_transform(plan._h, ctypes.c_void_p(M.data_ptr()),
-                                                                  ctypes.byref(yt), sh),
     }
+    if fused:
+        stages["contract_output"] = lambda: lib.winograd_contract_output(
+            plan._h, ctypes.c_void_p(V.data_ptr()), ctypes.c_void_p(U.data_ptr()), C, ctypes.byref(yt), sh)
+    else:
+        stages["contract"] = lambda: lib.winograd_contract(plan._h, ctypes.c_void_p(V.data_ptr()),
+                                                           ctypes.c_void_p(U.data_ptr()),
+                                                           ctypes.c_void_p(M.data_ptr()), g["T"], C, K, sh)
+        stages["output_transform"] = lambda: lib.winograd_output_transform(
+            plan._h, ctypes.c_void_p(M.data_ptr()), ctypes.byref(yt), sh)
+    return stages
 
 
 def time_kernels(stages, reps, stream):
@@ -107,12 +119,11 @@ def time_kernels(stages, reps, stream):
     launches on ``stream``, bracketed by HIP events."""
     import torch
     from paper_1905_05233_amd import _native as NAT
-    for name in KERNEL_NAMES:
-        NAT.check(stages[name]())
+    for fn in stages.values():
+        NAT.check(fn())
     torch.cuda.synchronize()
     out = {}
-    for name in KERNEL_NAMES:
-        fn = stages[name]
+    for name, fn in stages.items():
         for _ in range(3):
             fn()
         k0 = torch.cuda.Event(enable_timing=True)
@@ -128,7 +139,7 @@ def time_kernels(stages, reps, stream):
 
 def roofline(dom, work, us, dtype):
     """Roofline record of kernel ``dom`` from its algorithmic work and time."""
-    if dom == "contract":
+    if dom in ("contract", "contract_output"):
         ai = work["flops"] / work["bytes"]
         ridge = MFMA_PEAK_TFLOPS[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
         if ai >= ridge:
@@ -185,20 +196,24 @@ def run_vgg(a):
         kus = time_kernels(stages, reps, stream)
         wl = WL.Workload(f"vgg{i}", N=N, H=hw, W=hw, C=C, K=K, dtype=dtype, plans=(), x_dist="halfnormal")
         work = algorithmic_work(wl, L["plan"].alpha, L["plan"].m)
-        for k in KERNEL_NAMES:
+        for k in kus:
             tot_us[k] += kus[k]
             tot_work[k]["bytes"] += work[k]["bytes"]
             tot_work[k]["flops"] += work[k].get("flops", 0)
         layers.append({"layer": i, "H": hw, "C": C, "K": K, "moduli": L["spec"].moduli, "m": L["spec"].m,
-                       "alpha": L["plan"].alpha, "conv_ms": round(float(per_layer[i]), 4),
+                       "alpha": L["plan"].alpha, "path": L["plan"].conv_path(N, hw, hw, C, K),
+                       "conv_ms": round(float(per_layer[i]), 4),
                        "kernels_us": {k: round(v, 2) for k, v in kus.items()}})
         xi = relu_pool(y, L["pool"])
     dom = max(KERNEL_NAMES, key=lambda k: tot_us[k])
     roof = roofline(dom, tot_work[dom], tot_us[dom], dtype)
     roof["traffic"] = None
+    used = [k for k in KERNEL_NAMES if tot_us[k] > 0]
     kernels = {k: {"total_us": round(tot_us[k], 2), "algorithmic_bytes": tot_work[k]["bytes"],
-                   "GB_s": round(tot_work[k]["bytes"] / (tot_us[k] * 1e-6) / 1e9, 1)} for k in KERNEL_NAMES}
-    kernels["contract"]["TFLOP_s"] = round(tot_work["contract"]["flops"] / (tot_us["contract"] * 1e-6) / 1e12, 2)
+                   "GB_s": round(tot_work[k]["bytes"] / (tot_us[k] * 1e-6) / 1e9, 1)} for k in used}
+    for k in ("contract", "contract_output"):
+        if k in kernels:
+            kernels[k]["TFLOP_s"] = round(tot_work[k]["flops"] / (tot_us[k] * 1e-6) / 1e12, 2)
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s (direct-equivalent)",
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 5),
@@ -300,8 +315,11 @@ def main(argv=None):
                           "bytes_written_per_launch": dst.numel() * 4, "launches": a.steps}))
         return 0
     if a.profile_kernel:
-        for name in KERNEL_NAMES:       # produce valid inputs for the profiled kernel
-            NAT.check(stages[name]())
+        if a.profile_kernel not in stages:
+            print(f"bench.py: {a.profile_kernel} is not on this layer's path ({list(stages)})", file=sys.stderr)
+            return 2
+        for fn in stages.values():      # produce valid inputs for the profiled kernel
+            NAT.check(fn())
         torch.cuda.synchronize()
         for _ in range(a.steps):
             NAT.check(stages[a.profile_kernel]())
@@ -340,7 +358,7 @@ def main(argv=None):
 
     wtag = a.workload + (f"p{a.plan}" if a.plan else "")
     kernels = {}
-    for name in KERNEL_NAMES:
+    for name in stages:
         us = kernel_us[name]
         rec = {"avg_us": round(us, 3), "algorithmic_bytes": work[name]["bytes"],
                "GB_s": round(work[name]["bytes"] / (us * 1e-6) / 1e9, 1)}
@@ -348,7 +366,7 @@ def main(argv=None):
             rec["algorithmic_flops"] = work[name]["flops"]
             rec["TFLOP_s"] = round(work[name]["flops"] / (us * 1e-6) / 1e12, 2)
         kernels[name] = rec
-    dom = max(KERNEL_NAMES, key=lambda n: kernel_us[n])
+    dom = max(stages, key=lambda n: kernel_us[n])
     roof = roofline(dom, work[dom], kernel_us[dom], wl.dtype)
     roof["traffic"] = load_traffic(dom, wtag)
 
@@ -364,7 +382,8 @@ def main(argv=None):
         "config": {"workload": f"conv3x3 s1 p1 NHWC N={wl.N} C={wl.C} K={wl.K} H=W={wl.H} {wl.dtype} "
                                f"F({ps.m}x{ps.m},3x3) moduli {{{ps.moduli}}}",
                    "N": wl.N, "H": wl.H, "W": wl.W, "C": wl.C, "K": wl.K, "moduli": ps.moduli, "m": ps.m,
-                   "alpha": plan.alpha, "tiles": work["T"], "graph": bool(a.graph)},
+                   "alpha": plan.alpha, "tiles": work["T"], "graph": bool(a.graph),
+                   "path": plan.conv_path(wl.N, wl.H, wl.W, wl.C, wl.K)},
         "kernels": kernels, "roofline": roof,
     }
     if a.cpu_seconds > 0:

@@ -114,12 +114,24 @@ wg_status winograd_plan_create_str(const char* moduli, const char* inner, int m,
  * linear points the second gives the matrices of Lavin & Gray's F(4,3). */
 typedef enum { WG_FACTORS_IN_B = 0, WG_FACTORS_IN_G = 1 } wg_crt_factors;
 
+/* How winograd_conv2d evaluates eq. (2) after the two transforms.
+ * WG_PATH_SEPARATE: the alpha'^2 channel contractions write M to the
+ * workspace and the output transform reads it back (four kernels).
+ * WG_PATH_FUSED: one kernel contracts and applies the output transform while
+ * M of each domain point is still in registers, so M never reaches memory
+ * (input tiles up to 8, i.e. m <= 6, and per-plane sizes of V and U under
+ * 4 GiB).  WG_PATH_AUTO picks per layer shape (winograd_conv_path reports
+ * the choice).  Both paths give results within the same error bound; they
+ * may differ in the last bits because the channel sums run in another order. */
+typedef enum { WG_PATH_AUTO = 0, WG_PATH_SEPARATE = 1, WG_PATH_FUSED = 2 } wg_conv_path;
+
 typedef struct {
     wg_crt_factors factors;
+    wg_conv_path path;
 } wg_plan_options;
 
 /* winograd_plan_create_str with options (opts == NULL means all defaults:
- * WG_FACTORS_IN_B).  An unknown option value is WG_ERR_ARG. */
+ * WG_FACTORS_IN_B, WG_PATH_AUTO).  An unknown option value is WG_ERR_ARG. */
 wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, int r, wg_dtype dtype,
                                   const wg_plan_options* opts, wg_plan* out);
 
@@ -143,17 +155,25 @@ wg_status winograd_plan_matrix_f32(wg_plan plan, char which, float* out, size_t 
  * Table 1), as an exact fraction. */
 wg_status winograd_plan_ratio(wg_plan plan, int64_t* num, int64_t* den);
 
-/* Device workspace needed by winograd_conv2d for this layer shape. */
+/* Device workspace needed by winograd_conv2d for this layer shape (U and V,
+ * plus M on the separate path). */
 wg_status winograd_workspace_bytes(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C,
                                    int64_t K, size_t* bytes);
+
+/* The path winograd_conv2d takes for this layer shape: WG_PATH_SEPARATE or
+ * WG_PATH_FUSED.  WG_ERR_UNSUPPORTED if the plan asks for WG_PATH_FUSED and
+ * the shape does not allow it. */
+wg_status winograd_conv_path(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C, int64_t K,
+                             wg_conv_path* path);
 
 /* Bind a caller-owned device workspace (256-byte aligned) to the plan; a
  * NULL pointer unbinds.  The plan keeps the pointer, not the memory. */
 wg_status winograd_plan_set_workspace(wg_plan plan, void* dev_ptr, size_t bytes);
 
 /* y = conv3x3(x, w) by eq. (2): launches the kernel transform, the input
- * transform, the alpha'^2 batched channel contraction and the output
- * transform on `stream`, using the bound workspace.  x is [N][H][W][C],
+ * transform, then the alpha'^2 batched channel contraction and the output
+ * transform (separate path) or the fused kernel that does both (fused path)
+ * on `stream`, using the bound workspace.  x is [N][H][W][C],
  * w is [K][3][3][C], y is [N][H][W][K]; N, H, W, C, K >= 1 (y->c = K). */
 wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
                           hipStream_t stream);
@@ -182,6 +202,13 @@ wg_status winograd_contract(wg_plan plan, const void* V, const void* U, float* M
 
 /* y[n][ty*m+o][tx*m+p][k] = (A^T M_tk A)[o][p], stored only inside H x W. */
 wg_status winograd_output_transform(wg_plan plan, const float* M, wg_tensor* y, hipStream_t stream);
+
+/* The fused path's kernel: y = output transform of the contraction of V and U
+ * (the two calls above) without M in memory; C is the input channel count
+ * (V and U rows hold Cp channels), y gives N, H, W and K.  WG_ERR_UNSUPPORTED
+ * for input tiles over 8 or per-plane sizes of V or U of 4 GiB or more. */
+wg_status winograd_contract_output(wg_plan plan, const void* V, const void* U, int64_t C, wg_tensor* y,
+                                   hipStream_t stream);
 
 /* Message describing the last error of the calling thread ("" if none). */
 const char* winograd_last_error(void);

@@ -27,10 +27,12 @@ class WgPolySet(ctypes.Structure):
 
 
 class WgPlanOptions(ctypes.Structure):
-    _fields_ = [("factors", ctypes.c_int)]
+    _fields_ = [("factors", ctypes.c_int), ("path", ctypes.c_int)]
 
 
 FACTOR_CODES = {"B": 0, "G": 1}
+PATH_CODES = {"auto": 0, "separate": 1, "fused": 2}
+PATH_NAMES = {v: k for k, v in PATH_CODES.items()}
 
 
 class WgTensor(ctypes.Structure):
@@ -75,12 +77,14 @@ def lib():
         "winograd_plan_ratio": (ctypes.c_int, [P, ctypes.POINTER(i64), ctypes.POINTER(i64)]),
         "winograd_workspace_bytes": (ctypes.c_int, [P, i64, i64, i64, i64, i64, ctypes.POINTER(sz)]),
         "winograd_plan_set_workspace": (ctypes.c_int, [P, P, sz]),
+        "winograd_conv_path": (ctypes.c_int, [P, i64, i64, i64, i64, i64, ctypes.POINTER(ctypes.c_int)]),
         "winograd_conv2d": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),
                                            ctypes.POINTER(WgTensor), P]),
         "winograd_kernel_transform": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), P, P]),
         "winograd_input_transform": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), P, P]),
         "winograd_contract": (ctypes.c_int, [P, P, P, P, i64, i64, i64, P]),
         "winograd_output_transform": (ctypes.c_int, [P, P, ctypes.POINTER(WgTensor), P]),
+        "winograd_contract_output": (ctypes.c_int, [P, P, P, i64, ctypes.POINTER(WgTensor), P]),
         "winograd_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sigs.items():

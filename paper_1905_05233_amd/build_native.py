@@ -34,6 +34,9 @@ UNITS = [
     ("transforms.hip", DEVICE + ["-DWG_DTYPE=0"], "transforms_f32.o"),
     ("transforms.hip", DEVICE + ["-DWG_DTYPE=1"], "transforms_f16.o"),
     ("transforms.hip", DEVICE + ["-DWG_DTYPE=2"], "transforms_bf16.o"),
+    ("fused.hip", DEVICE + ["-DWG_DTYPE=0"], "fused_f32.o"),
+    ("fused.hip", DEVICE + ["-DWG_DTYPE=1"], "fused_f16.o"),
+    ("fused.hip", DEVICE + ["-DWG_DTYPE=2"], "fused_bf16.o"),
 ]
 
 

@@ -18,6 +18,7 @@
 struct wg_plan_s {
     wg::Transforms tr;
     int dtype = 0;
+    int path = WG_PATH_AUTO;
     void* ws = nullptr;
     size_t ws_bytes = 0;
     wg::InputTable itab{};
@@ -84,8 +85,38 @@ wg_status check_create_args(int m, int r, wg_dtype dtype, wg_plan* out) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+bool fused_supported(int dt, const wg::Geometry& g) {
+    switch (dt) {
+        case 0: return wg::contract_output_supported_t<0>(g);
+        case 1: return wg::contract_output_supported_t<1>(g);
+        default: return wg::contract_output_supported_t<2>(g);
+    }
+}
+
+// The path winograd_conv2d takes; -1 if the plan asks for the fused path and
+// the shape does not allow it.
+//
+// The automatic choice follows where each path spends its time.  The separate
+// path moves 8 bytes of M per (tile, output channel, domain point) through
+// HBM; the fused kernel instead streams one 128-byte slice of every channel
+// row per domain point through LDS for each block of 2048 (tile, channel)
+// pairs, and each such step costs about as much as 8 bytes of M per pair when
+// rows are longer than two slices (measured on VGG-16 layer shapes).  It also
+// needs enough pair blocks to occupy every CU twice.  Hence: fused when a
+// channel row fits two slices (C <= 64 fp32, C <= 128 fp16/bf16) and there
+// are at least 2^20 pairs.  The rule uses no device query, so the workspace
+// size it implies is the same on every machine.
+int resolve_path(const wg_plan_s* p, const wg::Geometry& g) {
+    const bool ok = fused_supported(p->dtype, g);
+    if (p->path == WG_PATH_FUSED) return ok ? WG_PATH_FUSED : -1;
+    if (p->path == WG_PATH_SEPARATE || !ok) return WG_PATH_SEPARATE;
+    const int64_t row_bytes = g.Cp * wg::dtype_bytes(p->dtype);
+    return row_bytes <= 256 && g.T * g.K >= (int64_t(1) << 20) ? WG_PATH_FUSED : WG_PATH_SEPARATE;
+}
+
 struct Layout {
     wg::Geometry g;
+    int path;
     size_t u_off, v_off, m_off, total;
 };
 
@@ -94,6 +125,7 @@ size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 Layout layout_for(const wg_plan_s* p, int64_t N, int64_t H, int64_t W, int64_t C, int64_t K) {
     Layout L;
     L.g = wg::make_geometry(N, H, W, C, K, p->tr.m, p->tr.alpha);
+    L.path = resolve_path(p, L.g);
     const size_t es = static_cast<size_t>(wg::dtype_bytes(p->dtype));
     const size_t a2 = static_cast<size_t>(p->tr.alpha) * static_cast<size_t>(p->tr.alpha);
     const size_t ub = a2 * static_cast<size_t>(K) * static_cast<size_t>(L.g.Cp) * es;
@@ -102,7 +134,7 @@ Layout layout_for(const wg_plan_s* p, int64_t N, int64_t H, int64_t W, int64_t C
     L.u_off = 0;
     L.v_off = align256(ub);
     L.m_off = L.v_off + align256(vb);
-    L.total = L.m_off + align256(mb);
+    L.total = L.m_off + (L.path == WG_PATH_FUSED ? 0 : align256(mb));   // no M on the fused path
     return L;
 }
 
@@ -155,6 +187,14 @@ hipError_t launch_ot(int dt, const wg::Geometry& g, const wg::OutputTable& t, co
         case 0: return wg::launch_output_transform_t<0>(g, t, M, y, s);
         case 1: return wg::launch_output_transform_t<1>(g, t, M, y, s);
         default: return wg::launch_output_transform_t<2>(g, t, M, y, s);
+    }
+}
+hipError_t launch_co(int dt, const wg::Geometry& g, const wg::OutputTable& t, const void* V, const void* U,
+                     void* y, hipStream_t s) {
+    switch (dt) {
+        case 0: return wg::launch_contract_output_t<0>(g, t, V, U, y, s);
+        case 1: return wg::launch_contract_output_t<1>(g, t, V, U, y, s);
+        default: return wg::launch_contract_output_t<2>(g, t, V, U, y, s);
     }
 }
 
@@ -225,12 +265,17 @@ wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, 
         const int factors = opts ? static_cast<int>(opts->factors) : WG_FACTORS_IN_B;
         if (factors != WG_FACTORS_IN_B && factors != WG_FACTORS_IN_G)
             return fail(WG_ERR_ARG, "unknown CRT factor placement");
+        const int path = opts ? static_cast<int>(opts->path) : WG_PATH_AUTO;
+        if (path != WG_PATH_AUTO && path != WG_PATH_SEPARATE && path != WG_PATH_FUSED)
+            return fail(WG_ERR_ARG, "unknown convolution path");
         const std::vector<wg::Modulus> mods = wg::parse_moduli(moduli);
         std::vector<wg::Rat> pts;
         bool inf = true;
         if (inner && inner[0] != '\0') wg::parse_points(inner, &pts, &inf);
         else pts = {wg::Rat(0), wg::Rat(-1)};
-        return finish_plan(wg::build_transforms(mods, pts, inf, m, r, factors == WG_FACTORS_IN_G), dtype, out);
+        s = finish_plan(wg::build_transforms(mods, pts, inf, m, r, factors == WG_FACTORS_IN_G), dtype, out);
+        if (s == WG_OK) (*out)->path = path;
+        return s;
     });
 }
 
@@ -282,7 +327,19 @@ wg_status winograd_workspace_bytes(wg_plan plan, int64_t N, int64_t H, int64_t W
                                    size_t* bytes) {
     if (!plan || !bytes) return fail(WG_ERR_ARG, "null argument");
     if (!dims_ok(N, H, W, C, K)) return fail(WG_ERR_ARG, "layer sizes must be in [1, 2^31)");
-    *bytes = layout_for(plan, N, H, W, C, K).total;
+    const Layout L = layout_for(plan, N, H, W, C, K);
+    if (L.path < 0) return fail(WG_ERR_UNSUPPORTED, "the fused path does not support this layer shape");
+    *bytes = L.total;
+    return WG_OK;
+}
+
+wg_status winograd_conv_path(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C, int64_t K,
+                             wg_conv_path* path) {
+    if (!plan || !path) return fail(WG_ERR_ARG, "null argument");
+    if (!dims_ok(N, H, W, C, K)) return fail(WG_ERR_ARG, "layer sizes must be in [1, 2^31)");
+    const int p = resolve_path(plan, wg::make_geometry(N, H, W, C, K, plan->tr.m, plan->tr.alpha));
+    if (p < 0) return fail(WG_ERR_UNSUPPORTED, "the fused path does not support this layer shape");
+    *path = static_cast<wg_conv_path>(p);
     return WG_OK;
 }
 
@@ -308,6 +365,7 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
         return fail(WG_ERR_ARG, "y must be [N][H][W][K]");
     if (!dims_ok(x->n, x->h, x->w, x->c, w->n)) return fail(WG_ERR_ARG, "layer sizes must be in [1, 2^31)");
     const Layout L = layout_for(plan, x->n, x->h, x->w, x->c, w->n);
+    if (L.path < 0) return fail(WG_ERR_UNSUPPORTED, "the fused path does not support this layer shape");
     if (!plan->ws) return fail(WG_ERR_WORKSPACE, "no workspace bound to the plan");
     if (plan->ws_bytes < L.total)
         return fail(WG_ERR_WORKSPACE, "workspace too small: need " + std::to_string(L.total) + " bytes");
@@ -318,6 +376,8 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
     const int dt = plan->dtype;
     if ((s = from_hip(launch_kt(dt, L.g, plan->ktab, w->data, U, stream), "kernel transform")) != WG_OK) return s;
     if ((s = from_hip(launch_it(dt, L.g, plan->itab, x->data, V, stream), "input transform")) != WG_OK) return s;
+    if (L.path == WG_PATH_FUSED)
+        return from_hip(launch_co(dt, L.g, plan->otab, V, U, y->data, stream), "fused contraction");
     if ((s = from_hip(launch_ct(dt, L.g, V, U, M, stream), "contraction")) != WG_OK) return s;
     return from_hip(launch_ot(dt, L.g, plan->otab, M, y->data, stream), "output transform");
 }
@@ -363,6 +423,20 @@ wg_status winograd_output_transform(wg_plan plan, const float* M, wg_tensor* y, 
     if (!dims_ok(y->n, y->h, y->w, 1, y->c)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
     const wg::Geometry g = wg::make_geometry(y->n, y->h, y->w, 1, y->c, plan->tr.m, plan->tr.alpha);
     return from_hip(launch_ot(plan->dtype, g, plan->otab, M, y->data, stream), "output transform");
+}
+
+wg_status winograd_contract_output(wg_plan plan, const void* V, const void* U, int64_t C, wg_tensor* y,
+                                   hipStream_t stream) {
+    wg_status s = check_plan(plan);
+    if (s != WG_OK) return s;
+    if ((s = check_tensor(y, "y")) != WG_OK) return s;
+    if (!V || !U || !aligned16(V) || !aligned16(U))
+        return fail(WG_ERR_ARG, "V and U must be 16-byte aligned device pointers");
+    if (!dims_ok(y->n, y->h, y->w, C, y->c)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
+    const wg::Geometry g = wg::make_geometry(y->n, y->h, y->w, C, y->c, plan->tr.m, plan->tr.alpha);
+    if (!fused_supported(plan->dtype, g))
+        return fail(WG_ERR_UNSUPPORTED, "the fused kernel does not support this layer shape");
+    return from_hip(launch_co(plan->dtype, g, plan->otab, V, U, y->data, stream), "fused contraction");
 }
 
 const char* winograd_last_error(void) { return g_last_error.c_str(); }

@@ -196,16 +196,6 @@ constexpr int stream_sets(int nch) { return nch >= 8 ? 2 : 4; }
 constexpr int stream_threads(int nch) { return (kStreamMmaWaves + stream_loaders(nch)) * 64; }
 constexpr int kStreamRows = 32;
 constexpr int kStreamCols = kStreamMmaWaves * 16;
-constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw 32-bit buffer, gfx9 family
-constexpr uint32_t kOob = 0xfffffff0u;         // an offset beyond every record count used here
-
-// Buffer descriptor over [base, base + bytes), bytes clipped to [0, 2^32 - 1].
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
-    const int64_t n = bytes < 0 ? 0 : (bytes > 0xffffffffLL ? 0xffffffffLL : bytes);
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
-                                             static_cast<int>(static_cast<uint32_t>(n)),
-                                             static_cast<int>(kRsrcWord3));
-}
 
 template <int D> __device__ __forceinline__ void mma16_chunk(const u32x4& a, const u32x4& b, f32x4& c);
 
@@ -439,17 +429,6 @@ __global__ __launch_bounds__(stream_threads(NCH), 1) void contract_stream_kernel
     }
 }
 
-int device_cu_count() {
-    static int cache[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cache[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-        cache[dev] = n;
-    }
-    return cache[dev];
-}
 
 template <int D, int NCH>
 hipError_t launch_stream(const Geometry& g, const void* V, const void* U, float* M, int64_t row_bytes,
@@ -466,6 +445,18 @@ hipError_t launch_stream(const Geometry& g, const void* V, const void* U, float*
 }
 
 }  // namespace
+
+int device_cu_count() {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
 
 template <int D>
 hipError_t launch_contract_t(const Geometry& g, const void* V, const void* U, float* M, hipStream_t stream) {

@@ -40,4 +40,17 @@ template <> struct DTypeOf<0> { using type = float; };
 template <> struct DTypeOf<1> { using type = _Float16; };
 template <> struct DTypeOf<2> { using type = bf16_t; };
 
+// Buffer descriptors (gfx950): loads at an offset past the record count return
+// zero and stores there are dropped, which clips ragged tails without branches.
+constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw 32-bit buffer, gfx9 family
+constexpr uint32_t kOob = 0xfffffff0u;         // an offset beyond every record count used here
+
+// Buffer descriptor over [base, base + bytes), bytes clipped to [0, 2^32 - 1].
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+    const int64_t n = bytes < 0 ? 0 : (bytes > 0xffffffffLL ? 0xffffffffLL : bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                             static_cast<int>(static_cast<uint32_t>(n)),
+                                             static_cast<int>(kRsrcWord3));
+}
+
 }  // namespace wg

@@ -1,0 +1,403 @@
+// Contraction fused with the output transform (gfx950 matrix cores).
+//
+// eq. (2) of Barabasz & Gregg (arXiv 1905.05233) gives an output tile as
+// A^T [ sum_c (G g_c G^T) . (B^T d_c B) ] A, the product taken elementwise.
+// The separate path writes the channel sums M[xi][t][k] of all alpha'^2 domain
+// points xi to memory and reads them back in the output transform.  Here a
+// workgroup owns a block of (output channel, tile) pairs for every xi: the
+// MFMAs leave M of one xi = (a, b) in the accumulators, and it is folded into
+// the output tile at once,
+//
+//     Z[o]     = sum_a A^T[o][a] M[a][b]      (a ascending: the xi loop runs a fastest)
+//     Y[o][p] += Z[o] A^T[p][b]               (after the last a of column b; b ascending)
+//
+// which is the order of operations of the stand-alone output transform, so
+// M never reaches memory.  The MFMA rows are output channels (U) and its
+// columns are tiles (V): a lane's accumulator then holds four consecutive
+// channels of one tile, written as one 8- or 16-byte NHWC store per pixel.
+//
+// Workgroup: four waves of 16 channels x 16*WT tiles each, kw waves side by
+// side along the channels and 4/kw along the tiles.  A step covers one
+// 128-byte slice of the channel rows of one xi: the block's U and V rows are
+// staged in double-buffered LDS (rows padded to 144 bytes, so the 16-byte
+// fragment reads are conflict-free), with the next step's global loads in
+// flight during the current MFMAs.  Global loads go through buffer
+// descriptors clipped to the plane, so rows past T or K and bytes past a row
+// read as zero.
+#include <algorithm>
+
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+#ifndef WG_DTYPE
+#error "compile once per storage dtype with -DWG_DTYPE=0 (fp32), 1 (fp16) or 2 (bf16)"
+#endif
+
+namespace wg {
+
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kThreads = 256;
+constexpr int kSlice = 128;                          // bytes of each channel row per step
+// LDS rows per stage: 16 kw channel rows + 16 WT (4 / kw) tile rows, at most
+// 96 (kw >= 2 when WT = 2), filled by 12 DMA instructions of 8 rows
+constexpr int kStageRows = 96;
+constexpr int kDmaPerWave = kStageRows / 8 / 4;      // per wave and step
+constexpr int kStageBytes = kStageRows * kSlice;
+
+// One 16-byte fragment pair: lanes of group g hold the same slice of the
+// channel range on both operands, so every channel meets its partner.
+template <int D>
+__device__ __forceinline__ void mma(const u32x4& a, const u32x4& b, f32x4& c) {
+    if constexpr (D == 0) {
+        const f32x4 av = __builtin_bit_cast(f32x4, a);
+        const f32x4 bv = __builtin_bit_cast(f32x4, b);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], bv[e], c, 0, 0, 0);
+    } else if constexpr (D == 1) {
+        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
+                                                   0, 0, 0);
+    } else {
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                    c, 0, 0, 0);
+    }
+}
+
+template <typename Elem> __device__ __forceinline__ uint32_t bits16(Elem v) {
+    if constexpr (sizeof(Elem) == 2 && __is_same(Elem, bf16_t)) return v.bits;
+    else return __builtin_bit_cast(uint16_t, v);
+}
+
+// four consecutive output channels of one pixel, rounded to the storage dtype
+template <typename Elem>
+__device__ __forceinline__ void store4(Elem* dst, float v0, float v1, float v2, float v3) {
+    using S = Storage<Elem>;
+    if constexpr (sizeof(Elem) == 4) {
+        *reinterpret_cast<f32x4*>(dst) = f32x4{v0, v1, v2, v3};
+    } else {
+        const uint32_t lo = bits16(S::from_f32(v0)) | (bits16(S::from_f32(v1)) << 16);
+        const uint32_t hi = bits16(S::from_f32(v2)) | (bits16(S::from_f32(v3)) << 16);
+        *reinterpret_cast<u32x2*>(dst) = u32x2{lo, hi};
+    }
+}
+
+// 16 bytes per lane from a buffer straight into LDS (no registers): lane l
+// lands at dst + 16 l; offsets past the record count write zeros
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, unsigned char* dst, uint32_t voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, voff, 0, 0, 0);
+}
+
+// Workgroup barrier without the release fence of __syncthreads (which would
+// wait for every DMA in flight): the LDS the waves read next was filled by
+// DMAs that each wave has already waited for.  The empty asm statements keep
+// the compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// 16-byte LDS read issued from inline assembly, so the compiler does not
+// insert its own wait for the DMAs in flight (it cannot tell the stages
+// apart across iterations); the caller waits with lds_settle before use.
+__device__ __forceinline__ u32x4 lds_read16(const unsigned char* p) {
+    const uint32_t a = static_cast<uint32_t>(
+        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const unsigned char*)p));
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+    return v;
+}
+
+// wait for this wave's LDS reads; the operands tie the values to the wait
+__device__ __forceinline__ void lds_settle(u32x4& a, u32x4& b, u32x4& c, u32x4& d) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : : "memory");
+}
+
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding (gfx9 encoding; expcnt and lgkmcnt not waited on)
+constexpr int vm_wait(int n) { return (n & 0xf) | (0x7 << 4) | (0xf << 8) | (((n >> 4) & 0x3) << 14); }
+
+template <int D, int MM, int ALPHA, int WT>
+__global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
+    const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, typename DTypeOf<D>::type* __restrict__ y,
+    OutputTable tab, Geometry geo, int kw, int n_kb, int rb, int n_slices) {
+    using Elem = typename DTypeOf<D>::type;
+    using S = Storage<Elem>;
+    // four LDS stages (one step each, three steps in flight), separate arrays
+    // so that the compiler can tell the stage being read from the ones being
+    // filled
+    __shared__ __attribute__((aligned(1024))) unsigned char st0[kStageBytes];
+    __shared__ __attribute__((aligned(1024))) unsigned char st1[kStageBytes];
+    __shared__ __attribute__((aligned(1024))) unsigned char st2[kStageBytes];
+    __shared__ __attribute__((aligned(1024))) unsigned char st3[kStageBytes];
+
+    // XCD-aware numbering: the hardware deals consecutive workgroup ids
+    // round-robin over the 8 XCDs; give each XCD a contiguous run of units, so
+    // the channel blocks of one tile block share an L2
+    const int64_t G = gridDim.x;
+    const int64_t bid = blockIdx.x;
+    const int64_t xcd = bid % 8;
+    const int64_t unit = xcd * (G / 8) + std::min<int64_t>(xcd, G % 8) + bid / 8;
+    const int kb = static_cast<int>(unit % n_kb);
+    const int64_t tb = unit / n_kb;
+
+    const int krows = 16 * kw;              // channel rows of the block
+    const int vrows = 16 * WT * (4 / kw);   // tile rows of the block
+    const int rows = krows + vrows;         // <= kStageRows
+    const int64_t k0 = static_cast<int64_t>(kb) * krows;
+    const int64_t t0 = tb * vrows;
+    const int64_t T = geo.T, K = geo.K;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wk = wave % kw;               // channel block of this wave
+    const int wt = wave / kw;               // tile block of this wave
+    const int grp = lane >> 4;
+    const int l16 = lane & 15;
+
+    // DMA map: instruction j of wave w fills stage rows 8 (w + 4 j) .. + 7
+    // (channel rows first, then tile rows; whole instructions, since both
+    // counts are multiples of 16, so the choice of operand is uniform).  Lane l
+    // lands at row 8 (w + 4 j) + l / 8, 16-byte column l % 8, and fetches the
+    // row's piece (l % 8) ^ (l / 8): an XOR swizzle that keeps the fragment
+    // reads conflict-free without padding.  Instructions past the block's rows
+    // write zeros (every wave issues the same count, so one vmcnt fits all).
+    const int piece = ((lane & 7) ^ (lane >> 3)) * 16;
+    uint32_t roff[kDmaPerWave];
+    bool live[kDmaPerWave], isu[kDmaPerWave];
+#pragma unroll
+    for (int j = 0; j < kDmaPerWave; ++j) {
+        const int r8 = 8 * (wave + 4 * j);
+        live[j] = r8 < rows;
+        isu[j] = r8 < krows;
+        const int row = r8 + (lane >> 3);
+        roff[j] = static_cast<uint32_t>((row < krows ? row : row - krows) * rb + piece);
+    }
+    auto issue = [&](unsigned char* st, int xi, int sl, bool any) {
+        const auto ru = make_rsrc(U + (static_cast<int64_t>(xi) * K + k0) * rb, (K - k0) * rb);
+        const auto rv = make_rsrc(V + (static_cast<int64_t>(xi) * T + t0) * rb, (T - t0) * rb);
+        const int sb = sl * kSlice;
+        const bool in = any && sb + piece < rb;   // zero past the row
+#pragma unroll
+        for (int j = 0; j < kDmaPerWave; ++j)
+            dma16(isu[j] ? ru : rv, st + (wave + 4 * j) * 1024, live[j] && in ? roff[j] + sb : kOob);
+    };
+
+    f32x4 acc[WT];
+    float Z[WT][MM][4];
+    float Y[WT][MM][MM][4];
+#pragma unroll
+    for (int w = 0; w < WT; ++w) {
+        acc[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int o = 0; o < MM; ++o)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                Z[w][o][r] = 0.0f;
+#pragma unroll
+                for (int q = 0; q < MM; ++q) Y[w][o][q][r] = 0.0f;
+            }
+    }
+
+    // fragment addresses (row & 7 = l16 & 7 for both operands)
+    const int swz = l16 & 7;
+    const int a_row = (wk * 16 + l16) * kSlice;
+    const int b_row = (krows + wt * 16 * WT + l16) * kSlice;
+    const int col0 = ((grp) ^ swz) * 16;       // slice half 0: pieces 0..3
+    const int col1 = ((grp + 4) ^ swz) * 16;   // slice half 1: pieces 4..7
+    const int nsteps = ALPHA * ALPHA * n_slices;
+    // step order: slices fastest, then a (M row), then b (M column)
+    int a = 0, bc = 0, sl = 0;      // step being computed
+    int na = 0, nb = 0, ns = 0;     // next step to request
+    auto advance = [&](int& a_, int& b_, int& s_) {
+        if (++s_ == n_slices) {
+            s_ = 0;
+            if (++a_ == ALPHA) {
+                a_ = 0;
+                ++b_;
+            }
+        }
+    };
+    auto request = [&](unsigned char* st) {
+        // past the last step the group is issued anyway (all zeros), which
+        // keeps the outstanding count per step constant
+        const bool any = nb < ALPHA;
+        issue(st, any ? na * ALPHA + nb : 0, any ? ns : 0, any);
+        if (any) advance(na, nb, ns);
+    };
+
+    auto step = [&](const unsigned char* cur, unsigned char* nxt) {
+        // this wave's DMAs for `cur` are done once at most two groups remain;
+        // the barrier makes every wave's visible and frees `nxt` (read in the
+        // previous step) for the next request
+        __builtin_amdgcn_s_waitcnt(vm_wait(2 * kDmaPerWave));
+        lds_barrier();
+        request(nxt);
+        // two-level channel sum: each slice into a fresh accumulator, added
+        // to the running sum (a sequential chain over C would be C/4 deep)
+        f32x4 part[WT];
+#pragma unroll
+        for (int w = 0; w < WT; ++w) part[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        u32x4 fa0 = lds_read16(cur + a_row + col0);
+        u32x4 fa1 = lds_read16(cur + a_row + col1);
+        u32x4 fb[WT][2];
+#pragma unroll
+        for (int w = 0; w < WT; ++w) {
+            fb[w][0] = lds_read16(cur + b_row + w * 16 * kSlice + col0);
+            fb[w][1] = lds_read16(cur + b_row + w * 16 * kSlice + col1);
+        }
+        if constexpr (WT == 2) lds_settle(fa0, fa1, fb[0][0], fb[1][1]), lds_settle(fb[0][1], fb[1][0], fa0, fa1);
+        else lds_settle(fa0, fa1, fb[0][0], fb[0][1]);
+#pragma unroll
+        for (int w = 0; w < WT; ++w) {
+            mma<D>(fa0, fb[w][0], part[w]);
+            mma<D>(fa1, fb[w][1], part[w]);
+        }
+#pragma unroll
+        for (int w = 0; w < WT; ++w) acc[w] += part[w];
+        if (sl == n_slices - 1) {
+            // M[a][bc] of this block is complete: fold it into Z (pass 1)
+#pragma unroll
+            for (int o = 0; o < MM; ++o) {
+                const float c = tab.at[o * ALPHA + a];
+#pragma unroll
+                for (int w = 0; w < WT; ++w)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) Z[w][o][r] = __builtin_fmaf(c, acc[w][r], Z[w][o][r]);
+            }
+#pragma unroll
+            for (int w = 0; w < WT; ++w) acc[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            if (a == ALPHA - 1) {
+                // column bc done: pass 2 into the output tile
+#pragma unroll
+                for (int q = 0; q < MM; ++q) {
+                    const float c = tab.at[q * ALPHA + bc];
+#pragma unroll
+                    for (int w = 0; w < WT; ++w)
+#pragma unroll
+                        for (int o = 0; o < MM; ++o)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) Y[w][o][q][r] = __builtin_fmaf(Z[w][o][r], c, Y[w][o][q][r]);
+                }
+#pragma unroll
+                for (int w = 0; w < WT; ++w)
+#pragma unroll
+                    for (int o = 0; o < MM; ++o)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) Z[w][o][r] = 0.0f;
+            }
+        }
+        advance(a, bc, sl);
+    };
+
+    // prologue: steps 0, 1, 2 requested into stages 0, 1, 2
+    request(st0);
+    request(st1);
+    request(st2);
+    // step s reads stage s % 4 and requests step s + 3 into stage (s + 3) % 4
+    for (int s0 = 0; s0 < nsteps; s0 += 4) {
+        step(st0, st3);
+        if (s0 + 1 >= nsteps) break;
+        step(st1, st0);
+        if (s0 + 2 >= nsteps) break;
+        step(st2, st1);
+        if (s0 + 3 >= nsteps) break;
+        step(st3, st2);
+    }
+    // the trailing zero groups must land before the wave ends (the LDS of
+    // the workgroup is then handed to the next one)
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));
+
+    // epilogue: masked NHWC store, four consecutive channels per lane
+    const int64_t k = k0 + wk * 16 + 4 * grp;
+    if (k >= K) return;
+    const bool vec = (K & 3) == 0;
+#pragma unroll
+    for (int w = 0; w < WT; ++w) {
+        const int64_t tile = t0 + (wt * WT + w) * 16 + l16;
+        if (tile >= T) continue;
+        const int64_t tx = tile % geo.tw;
+        const int64_t ty = (tile / geo.tw) % geo.th;
+        const int64_t n = tile / (geo.tw * geo.th);
+#pragma unroll
+        for (int o = 0; o < MM; ++o) {
+            const int64_t hr = ty * MM + o;
+            if (hr >= geo.H) break;
+#pragma unroll
+            for (int q = 0; q < MM; ++q) {
+                const int64_t wc = tx * MM + q;
+                if (wc >= geo.W) break;
+                Elem* dst = y + ((n * geo.H + hr) * geo.W + wc) * K + k;
+                if (vec) {
+                    store4(dst, Y[w][o][q][0], Y[w][o][q][1], Y[w][o][q][2], Y[w][o][q][3]);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (k + r < K) dst[r] = S::from_f32(Y[w][o][q][r]);
+                }
+            }
+        }
+    }
+}
+
+// tile blocks per wave: as many as the output-tile registers allow (Y holds
+// m^2 values per channel-tile pair), fewer when that leaves CUs idle
+int pick_wt(const Geometry& g, int kw) {
+    if (g.m > 4) return 1;
+    const int64_t n_kb = (g.K + 16 * kw - 1) / (16 * kw);
+    const int64_t n_tb2 = (g.T + 16 * 2 * (4 / kw) - 1) / (16 * 2 * (4 / kw));
+    return n_kb * n_tb2 >= 2 * device_cu_count() ? 2 : 1;
+}
+
+}  // namespace
+
+template <>
+bool contract_output_supported_t<WG_DTYPE>(const Geometry& g) {
+    const int64_t rb = g.Cp * (WG_DTYPE == 0 ? 4 : 2);
+    if (g.t > 8 || !transform_shape_supported(g.t, g.alpha)) return false;
+    // 32-bit buffer offsets: within a plane, and for every staged row of a block
+    return g.T * rb < 0xffff0000LL && g.K * rb < 0xffff0000LL && rb <= (1 << 20);
+}
+
+template <>
+hipError_t launch_contract_output_t<WG_DTYPE>(const Geometry& g, const OutputTable& tab, const void* V,
+                                              const void* U, void* y, hipStream_t stream) {
+    constexpr int D = WG_DTYPE;
+    using Elem = typename DTypeOf<D>::type;
+    if (!contract_output_supported_t<D>(g)) return hipErrorInvalidValue;
+    const int rb = static_cast<int>(g.Cp * (D == 0 ? 4 : 2));
+    const int kw0 = g.K <= 16 ? 1 : g.K <= 32 ? 2 : 4;
+    const int wt = pick_wt(g, std::max(kw0, 2));
+    const int kw = wt == 2 ? std::max(kw0, 2) : kw0;   // a stage holds at most 96 rows
+    const int n_kb = static_cast<int>((g.K + 16 * kw - 1) / (16 * kw));
+    const int64_t n_tb = (g.T + 16 * wt * (4 / kw) - 1) / (16 * wt * (4 / kw));
+    const int64_t grid = n_kb * n_tb;
+    if (grid > 0x7fffffff) return hipErrorInvalidValue;
+    const int n_slices = (rb + kSlice - 1) / kSlice;
+    const auto* vp = static_cast<const unsigned char*>(V);
+    const auto* up = static_cast<const unsigned char*>(U);
+    auto* yp = static_cast<Elem*>(y);
+    const unsigned nb = static_cast<unsigned>(grid);
+#define WG_CO_CASE(TT, A, W)                                                                              \
+    if (g.t == TT && g.alpha == A && wt == W) {                                                           \
+        hipLaunchKernelGGL((contract_output_kernel<D, TT - 2, A, W>), dim3(nb), dim3(kThreads), 0, stream, vp, \
+                           up, yp, tab, g, kw, n_kb, rb, n_slices);                                       \
+        return hipGetLastError();                                                                         \
+    }
+    WG_CO_CASE(4, 4, 1) WG_CO_CASE(4, 5, 1) WG_CO_CASE(4, 6, 1) WG_CO_CASE(4, 7, 1)
+    WG_CO_CASE(4, 4, 2) WG_CO_CASE(4, 5, 2) WG_CO_CASE(4, 6, 2) WG_CO_CASE(4, 7, 2)
+    WG_CO_CASE(6, 6, 1) WG_CO_CASE(6, 7, 1) WG_CO_CASE(6, 8, 1) WG_CO_CASE(6, 9, 1)
+    WG_CO_CASE(6, 6, 2) WG_CO_CASE(6, 7, 2) WG_CO_CASE(6, 8, 2) WG_CO_CASE(6, 9, 2)
+    WG_CO_CASE(8, 8, 1) WG_CO_CASE(8, 9, 1) WG_CO_CASE(8, 10, 1) WG_CO_CASE(8, 11, 1) WG_CO_CASE(8, 12, 1)
+#undef WG_CO_CASE
+    return hipErrorInvalidValue;
+}
+
+}  // namespace wg

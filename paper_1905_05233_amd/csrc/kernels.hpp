@@ -74,4 +74,15 @@ hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, 
 template <int D>
 hipError_t launch_contract_t(const Geometry& g, const void* V, const void* U, float* M, hipStream_t stream);
 
+// Contraction fused with the output transform: V, U -> y with no M in memory.
+// Supported for input tiles up to 8 (m <= 6) and planes addressable with
+// 32-bit offsets; the launcher returns hipErrorInvalidValue otherwise.
+template <int D> bool contract_output_supported_t(const Geometry& g);
+template <int D>
+hipError_t launch_contract_output_t(const Geometry& g, const OutputTable& tab, const void* V, const void* U,
+                                    void* y, hipStream_t stream);
+
+// Compute units of the current device (cached per device).
+int device_cu_count();
+
 }  // namespace wg

@@ -37,24 +37,28 @@ def _tensor(t, name, shape=None):
 class Plan:
     """A Winograd plan F(m x m, 3 x 3) built from a modulus set (Algorithms 1, 2)."""
 
-    def __init__(self, moduli, m, dtype="f32", inner="0,-1,inf", r=3, factors="B"):
+    def __init__(self, moduli, m, dtype="f32", inner="0,-1,inf", r=3, factors="B", path="auto"):
         """``factors``: where the CRT factors N_i go, "B" (the paper's
-        matrices) or "G" (on the kernel residues)."""
+        matrices) or "G" (on the kernel residues).  ``path``: "separate"
+        (M through memory), "fused" (contraction and output transform in one
+        kernel) or "auto" (chosen per layer shape)."""
         if dtype not in N.DTYPE_CODES:
             raise ValueError(f"dtype must be one of {list(N.DTYPE_CODES)}")
         if factors not in N.FACTOR_CODES:
             raise ValueError(f"factors must be one of {list(N.FACTOR_CODES)}")
+        if path not in N.PATH_CODES:
+            raise ValueError(f"path must be one of {list(N.PATH_CODES)}")
         self._lib = N.lib()
         self._h = ctypes.c_void_p()
-        if factors == "B":
+        if factors == "B" and path == "auto":
             N.check(self._lib.winograd_plan_create_str(moduli.encode(), (inner or "").encode(), int(m), int(r),
                                                        N.DTYPE_CODES[dtype], ctypes.byref(self._h)))
         else:
-            opts = N.WgPlanOptions(N.FACTOR_CODES[factors])
+            opts = N.WgPlanOptions(N.FACTOR_CODES[factors], N.PATH_CODES[path])
             N.check(self._lib.winograd_plan_create_ex(moduli.encode(), (inner or "").encode(), int(m), int(r),
                                                       N.DTYPE_CODES[dtype], ctypes.byref(opts),
                                                       ctypes.byref(self._h)))
-        self.moduli, self.inner, self.dtype, self.factors = moduli, inner, dtype, factors
+        self.moduli, self.inner, self.dtype, self.factors, self.path = moduli, inner, dtype, factors, path
         vals = [ctypes.c_int() for _ in range(5)]
         N.check(self._lib.winograd_plan_info(self._h, *[ctypes.byref(v) for v in vals]))
         self.m, self.r, self.alpha, self.tile_in, _ = [v.value for v in vals]
@@ -84,7 +88,7 @@ class Plan:
         self._h = ctypes.c_void_p()
         N.check(self._lib.winograd_plan_create(ctypes.byref(ps), int(m), int(r), N.DTYPE_CODES[dtype],
                                                ctypes.byref(self._h)))
-        self.moduli, self.inner, self.dtype, self.factors = moduli, inner_points, dtype, "B"
+        self.moduli, self.inner, self.dtype, self.factors, self.path = moduli, inner_points, dtype, "B", "auto"
         vals = [ctypes.c_int() for _ in range(5)]
         N.check(self._lib.winograd_plan_info(self._h, *[ctypes.byref(v) for v in vals]))
         self.m, self.r, self.alpha, self.tile_in, _ = [v.value for v in vals]
@@ -119,6 +123,12 @@ class Plan:
         out = ctypes.c_size_t()
         N.check(self._lib.winograd_workspace_bytes(self._h, N_, H, W, C, K, ctypes.byref(out)))
         return out.value
+
+    def conv_path(self, N_, H, W, C, K):
+        """"separate" or "fused": the path conv2d takes for this layer shape."""
+        out = ctypes.c_int()
+        N.check(self._lib.winograd_conv_path(self._h, N_, H, W, C, K, ctypes.byref(out)))
+        return N.PATH_NAMES[out.value]
 
     # ------------------------------------------------------------- compute
     @property
@@ -229,6 +239,24 @@ class Plan:
                                                     _stream_handle(stream)))
         return y
 
+    def contract_output(self, V, U, C, N_, H, W, stream=None):
+        """The fused kernel alone: y [N][H][W][K] from V and U, no M in memory."""
+        self._check_dtype(V, "V")
+        self._check_dtype(U, "U")
+        a2, T, Cp = V.shape
+        K = U.shape[1]
+        g = self.geometry(N_, H, W, C, K)
+        if a2 != self.alpha ** 2 or U.shape[0] != a2 or U.shape[2] != Cp or Cp != g["Cp"] or T != g["T"]:
+            raise ValueError("V must be [alpha'^2][T][Cp] and U [alpha'^2][K][Cp]")
+        if not (V.is_contiguous() and U.is_contiguous()):
+            raise ValueError("V and U must be contiguous")
+        y = torch.empty((N_, H, W, K), dtype=self.torch_dtype, device=V.device)
+        yt = _tensor(y, "y")
+        N.check(self._lib.winograd_contract_output(self._h, ctypes.c_void_p(V.data_ptr()),
+                                                   ctypes.c_void_p(U.data_ptr()), C, ctypes.byref(yt),
+                                                   _stream_handle(stream)))
+        return y
+
     # ------------------------------------------------------------ lifetime
     def close(self):
         if getattr(self, "_h", None) and self._h.value:
@@ -242,4 +270,4 @@ class Plan:
             pass
 
     def __repr__(self):
-        return f"Plan({self.moduli!r}, m={self.m}, dtype={self.dtype!r}, alpha'={self.alpha})"
+        return f"Plan({self.moduli!r}, m={self.m}, dtype={self.dtype!r}, alpha'={self.alpha}, path={self.path!r})"

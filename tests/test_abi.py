@@ -160,8 +160,38 @@ def test_exact_overflow_is_reported():
     assert ei.value.status in (6,)
 
 
+def test_conv_path_option_and_workspace():
+    """WG_PATH_SEPARATE / WG_PATH_FUSED / WG_PATH_AUTO: the resolved path and
+    the workspace (the fused path needs no M), and the errors."""
+    Nn, H, W, C, K = 2, 20, 20, 16, 24
+    ps = Plan(WL.F4_LINEAR, m=4, path="separate")
+    pf = Plan(WL.F4_LINEAR, m=4, path="fused")
+    pa = Plan(WL.F4_LINEAR, m=4)
+    assert ps.conv_path(Nn, H, W, C, K) == "separate"
+    assert pf.conv_path(Nn, H, W, C, K) == "fused"
+    assert pa.conv_path(Nn, H, W, C, K) in ("separate", "fused")
+    T, a2, Kp = Nn * 5 * 5, 36, 24
+    m_bytes = -(-a2 * T * Kp * 4 // 256) * 256
+    assert ps.workspace_bytes(Nn, H, W, C, K) - pf.workspace_bytes(Nn, H, W, C, K) == m_bytes
+    # input tile 10 (m = 8): no fused kernel; asking for it is an error, auto takes the separate path
+    spec8 = "0,-1,1,-1/2,2,1/2,-2,a^2+1,inf"
+    big = Plan(spec8, m=8, path="fused")
+    for call in (big.conv_path, big.workspace_bytes):
+        with pytest.raises(N.WinogradError) as ei:
+            call(Nn, H, W, C, K)
+        assert ei.value.status == 5
+    assert Plan(spec8, m=8).conv_path(Nn, H, W, C, K) == "separate"
+    lib = N.lib()
+    h = ctypes.c_void_p()
+    bad = N.WgPlanOptions(0, 9)
+    assert lib.winograd_plan_create_ex(WL.F4_LINEAR.encode(), b"", 4, 3, 0, ctypes.byref(bad), ctypes.byref(h)) == 1
+    assert not h.value
+    with pytest.raises(ValueError):
+        Plan(WL.F4_LINEAR, m=4, path="fast")
+
+
 def test_workspace_bytes_and_errors():
-    p = Plan(WL.F4_LINEAR, m=4, dtype="f32")
+    p = Plan(WL.F4_LINEAR, m=4, dtype="f32", path="separate")
     Nn, H, W, C, K = 8, 56, 56, 128, 128
     T = Nn * 14 * 14
     need = p.workspace_bytes(Nn, H, W, C, K)
