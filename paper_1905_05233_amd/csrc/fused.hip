@@ -233,40 +233,33 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
         if (any) advance(na, nb, ns);
     };
 
-    auto step = [&](const unsigned char* cur, unsigned char* nxt) {
-        // this wave's DMAs for `cur` are done once at most two groups remain;
-        // the barrier makes every wave's visible and frees `nxt` (read in the
-        // previous step) for the next request
-        __builtin_amdgcn_s_waitcnt(vm_wait(2 * kDmaPerWave));
-        lds_barrier();
-        request(nxt);
-        // two-level channel sum: each slice into a fresh accumulator, added
-        // to the running sum (a sequential chain over C would be C/4 deep)
-        f32x4 part[WT];
+    // two-level channel sum: each step's slice goes into a fresh accumulator
+    // `part`, added to the running sum `acc` (a sequential chain over C would
+    // be C/4 deep).  The fold of a step into Z and Y runs one step later,
+    // while the next step's LDS reads are in flight, and consumes the MFMA
+    // results only then.
+    f32x4 part[WT];
 #pragma unroll
-        for (int w = 0; w < WT; ++w) part[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        u32x4 fa0 = lds_read16(cur + a_row + col0);
-        u32x4 fa1 = lds_read16(cur + a_row + col1);
-        u32x4 fb[WT][2];
+    for (int w = 0; w < WT; ++w) part[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    // the output-transform coefficients of the step being folded, A^T[o][a]
+    // and A^T[o][bc], are loaded into scalar registers before its LDS reads
+    // are issued (a wait for them afterwards would also wait for those reads)
+    float cz[MM], cy[MM];
+    auto coefs = [&]() __attribute__((always_inline)) {
 #pragma unroll
-        for (int w = 0; w < WT; ++w) {
-            fb[w][0] = lds_read16(cur + b_row + w * 16 * kSlice + col0);
-            fb[w][1] = lds_read16(cur + b_row + w * 16 * kSlice + col1);
+        for (int o = 0; o < MM; ++o) {
+            cz[o] = tab.at[o * ALPHA + a];
+            cy[o] = tab.at[o * ALPHA + bc];
         }
-        if constexpr (WT == 2) lds_settle(fa0, fa1, fb[0][0], fb[1][1]), lds_settle(fb[0][1], fb[1][0], fa0, fa1);
-        else lds_settle(fa0, fa1, fb[0][0], fb[0][1]);
-#pragma unroll
-        for (int w = 0; w < WT; ++w) {
-            mma<D>(fa0, fb[w][0], part[w]);
-            mma<D>(fa1, fb[w][1], part[w]);
-        }
+    };
+    auto fold = [&]() __attribute__((always_inline)) {   // the step (a, bc, sl)
 #pragma unroll
         for (int w = 0; w < WT; ++w) acc[w] += part[w];
         if (sl == n_slices - 1) {
             // M[a][bc] of this block is complete: fold it into Z (pass 1)
 #pragma unroll
             for (int o = 0; o < MM; ++o) {
-                const float c = tab.at[o * ALPHA + a];
+                const float c = cz[o];
 #pragma unroll
                 for (int w = 0; w < WT; ++w)
 #pragma unroll
@@ -278,7 +271,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
                 // column bc done: pass 2 into the output tile
 #pragma unroll
                 for (int q = 0; q < MM; ++q) {
-                    const float c = tab.at[q * ALPHA + bc];
+                    const float c = cy[q];
 #pragma unroll
                     for (int w = 0; w < WT; ++w)
 #pragma unroll
@@ -297,6 +290,38 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
         advance(a, bc, sl);
     };
 
+    bool have_prev = false;
+    auto step = [&](const unsigned char* cur, unsigned char* nxt) __attribute__((always_inline)) {
+        // this wave's DMAs for `cur` are done once at most two groups remain;
+        // the barrier makes every wave's visible and frees `nxt` (read in the
+        // previous step) for the next request
+        coefs();
+        __builtin_amdgcn_s_waitcnt(vm_wait(2 * kDmaPerWave));
+        lds_barrier();
+        request(nxt);
+        // the coefficients must be in registers before the LDS reads go out
+#pragma unroll
+        for (int o = 0; o < MM; ++o) asm volatile("" : "+s"(cz[o]), "+s"(cy[o]));
+        u32x4 fa0 = lds_read16(cur + a_row + col0);
+        u32x4 fa1 = lds_read16(cur + a_row + col1);
+        u32x4 fb[WT][2];
+#pragma unroll
+        for (int w = 0; w < WT; ++w) {
+            fb[w][0] = lds_read16(cur + b_row + w * 16 * kSlice + col0);
+            fb[w][1] = lds_read16(cur + b_row + w * 16 * kSlice + col1);
+        }
+        if (have_prev) fold();
+        have_prev = true;
+        if constexpr (WT == 2) lds_settle(fa0, fa1, fb[0][0], fb[1][1]), lds_settle(fb[0][1], fb[1][0], fa0, fa1);
+        else lds_settle(fa0, fa1, fb[0][0], fb[0][1]);
+#pragma unroll
+        for (int w = 0; w < WT; ++w) {
+            part[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            mma<D>(fa0, fb[w][0], part[w]);
+            mma<D>(fa1, fb[w][1], part[w]);
+        }
+    };
+
     // prologue: steps 0, 1, 2 requested into stages 0, 1, 2
     request(st0);
     request(st1);
@@ -311,6 +336,8 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
         if (s0 + 3 >= nsteps) break;
         step(st3, st2);
     }
+    coefs();
+    fold();   // the last step
     // the trailing zero groups must land before the wave ends (the LDS of
     // the workgroup is then handed to the next one)
     __builtin_amdgcn_s_waitcnt(vm_wait(0));
