@@ -34,43 +34,61 @@ constexpr int kBlock = 256;
 
 // ----------------------------------------------------------------- kernel
 // U[xi = a*alpha + b][k][c] = sum_j (sum_i G[a][i] g[i][j]) G[b][j]; one thread
-// per (row a, k, c), channel fastest.
-template <typename Elem, int ALPHA>
+// per (row a, k, 16-byte run of channels), runs fastest, so loads and stores
+// are 16 bytes per lane.  kWhole: C is a multiple of the run, so the runs of
+// w are 16-byte aligned; otherwise w is read element by element.
+template <typename Elem, int ALPHA, bool kWhole>
 __global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, const Elem* __restrict__ w,
                                                            Elem* __restrict__ U, int64_t K, int64_t C,
                                                            int64_t Cp) {
     using S = Storage<Elem>;
+    constexpr int kRun = 16 / static_cast<int>(sizeof(Elem));   // channels per thread
+    const int64_t runs = Cp / kRun;                              // Cp is a multiple of 8
     const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    if (gid >= ALPHA * K * Cp) return;
-    const int64_t c = gid % Cp;
-    const int64_t k = (gid / Cp) % K;
-    const int a = static_cast<int>(gid / (Cp * K));
+    if (gid >= ALPHA * K * runs) return;
+    const int64_t c = (gid % runs) * kRun;
+    const int64_t k = (gid / runs) % K;
+    const int a = static_cast<int>(gid / (runs * K));
     const int64_t plane = K * Cp;
-    Elem* out = U + static_cast<int64_t>(a) * ALPHA * plane + k * Cp + c;
-    if (c >= C) {
-#pragma unroll
-        for (int b = 0; b < ALPHA; ++b) out[b * plane] = S::from_f32(0.0f);
-        return;
-    }
-    float g[3][3];
+    float g[3][3][kRun];
 #pragma unroll
     for (int i = 0; i < 3; ++i)
 #pragma unroll
-        for (int j = 0; j < 3; ++j) g[i][j] = S::to_f32(w[((k * 3 + i) * 3 + j) * C + c]);
-    float Gg[3];
+        for (int j = 0; j < 3; ++j) {
+            const Elem* src = w + ((k * 3 + i) * 3 + j) * C + c;
+            Elem e[kRun];
+            if constexpr (kWhole) {
+                // a run starts inside C only if it ends inside it (for fp32, Cp may exceed C by a run)
+                *reinterpret_cast<uint4*>(e) = c < C ? *reinterpret_cast<const uint4*>(src) : uint4{0u, 0u, 0u, 0u};
+            } else {
 #pragma unroll
-    for (int j = 0; j < 3; ++j) {
-        float acc = 0.0f;
+                for (int q = 0; q < kRun; ++q) e[q] = c + q < C ? src[q] : S::from_f32(0.0f);
+            }
 #pragma unroll
-        for (int i = 0; i < 3; ++i) acc = __builtin_fmaf(tab.g[a * 3 + i], g[i][j], acc);
-        Gg[j] = acc;
-    }
+            for (int q = 0; q < kRun; ++q) g[i][j][q] = S::to_f32(e[q]);
+        }
+    float Gg[3][kRun];
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int q = 0; q < kRun; ++q) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 3; ++i) acc = __builtin_fmaf(tab.g[a * 3 + i], g[i][j][q], acc);
+            Gg[j][q] = acc;
+        }
+    Elem* out = U + static_cast<int64_t>(a) * ALPHA * plane + k * Cp + c;
 #pragma unroll
     for (int b = 0; b < ALPHA; ++b) {
-        float acc = 0.0f;
+        Elem e[kRun];
 #pragma unroll
-        for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(Gg[j], tab.g[b * 3 + j], acc);
-        out[b * plane] = S::from_f32(acc);
+        for (int q = 0; q < kRun; ++q) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(Gg[j][q], tab.g[b * 3 + j], acc);
+            e[q] = S::from_f32(acc);   // channels past C: g = 0, so zeros
+        }
+        *reinterpret_cast<uint4*>(out + b * plane) = *reinterpret_cast<const uint4*>(e);
     }
 }
 
@@ -308,12 +326,18 @@ hipError_t launch_kernel_transform_t(const Geometry& g, const KernelTable& tab, 
     using Elem = typename DTypeOf<D>::type;
     const auto* wp = static_cast<const Elem*>(w);
     auto* up = static_cast<Elem*>(U);
-    const unsigned nb = blocks_for(static_cast<int64_t>(g.alpha) * g.K * g.Cp);
+    constexpr int kRun = 16 / static_cast<int>(sizeof(Elem));
+    const unsigned nb = blocks_for(static_cast<int64_t>(g.alpha) * g.K * (g.Cp / kRun));
+    const bool whole = g.C % kRun == 0;
     switch (g.alpha) {
-#define WG_KT_CASE(A)                                                                             \
-    case A:                                                                                       \
-        hipLaunchKernelGGL((kernel_transform<Elem, A>), dim3(nb), dim3(kBlock), 0, stream, tab, wp, up, g.K, \
-                           g.C, g.Cp);                                                            \
+#define WG_KT_CASE(A)                                                                                   \
+    case A:                                                                                             \
+        if (whole)                                                                                      \
+            hipLaunchKernelGGL((kernel_transform<Elem, A, true>), dim3(nb), dim3(kBlock), 0, stream, tab, wp, up, \
+                               g.K, g.C, g.Cp);                                                         \
+        else                                                                                            \
+            hipLaunchKernelGGL((kernel_transform<Elem, A, false>), dim3(nb), dim3(kBlock), 0, stream, tab, wp, up, \
+                               g.K, g.C, g.Cp);                                                         \
         break;
         WG_KT_CASE(4) WG_KT_CASE(5) WG_KT_CASE(6) WG_KT_CASE(7) WG_KT_CASE(8) WG_KT_CASE(9)
         WG_KT_CASE(10) WG_KT_CASE(11) WG_KT_CASE(12) WG_KT_CASE(13) WG_KT_CASE(14) WG_KT_CASE(15)
