@@ -2,9 +2,9 @@
 """Throughput of the Winograd convolution hot path on one MI355X (gfx950).
 
 One step = one full layer through eq. (2) of Barabasz & Gregg (arXiv
-1905.05233): kernel transform, input transform, alpha'^2 batched matrix-core
-contraction and output transform (separate kernels, or the last two fused
-into one where the library picks that path for the layer shape), on seeded
+1905.05233): kernel and input transforms (one launch), alpha'^2 batched
+matrix-core contraction and output transform (separate kernels, or one fused
+kernel where the library picks that path for the layer shape), on seeded
 synthetic inputs already resident in HBM.  Default workload: conv3x3 stride 1 pad 1, N=8, C=K=128, H=W=56, fp32,
 F(4x4,3x3) with points {0, 1, -1, 1/2, -1/2, inf}.
 
@@ -34,10 +34,9 @@ if ROOT not in sys.path:
 METRIC = "direct-equiv conv TFLOP/s + MFMA util/HBM GB/s; rel-L2 err vs fp64 direct"
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0, "bf16": 2500.0}
-KERNEL_NAMES = ("kernel_transform", "input_transform", "contract", "output_transform", "contract_output")
-KERNEL_SOURCES = {"kernel_transform": "transforms.hip", "input_transform": "transforms.hip",
-                  "contract": "contract.hip", "output_transform": "transforms.hip",
-                  "contract_output": "fused.hip"}
+KERNEL_NAMES = ("kernel_input_transform", "contract", "output_transform", "contract_output")
+KERNEL_SOURCES = {"kernel_input_transform": "transforms.hip", "contract": "contract.hip",
+                  "output_transform": "transforms.hip", "contract_output": "fused.hip"}
 
 
 def algorithmic_work(wl, alpha, m):
@@ -48,8 +47,9 @@ def algorithmic_work(wl, alpha, m):
     a2 = alpha * alpha
     C, K = wl.C, wl.K
     return {
-        "kernel_transform": {"bytes": 9 * C * K * s + a2 * C * K * s},
-        "input_transform": {"bytes": wl.N * wl.H * wl.W * C * s + a2 * T * C * s},
+        # one launch: kernel transform (w in, U out) and input transform (x in, V out)
+        "kernel_input_transform": {"bytes": 9 * C * K * s + a2 * C * K * s + wl.N * wl.H * wl.W * C * s
+                                   + a2 * T * C * s},
         "contract": {"flops": 2 * a2 * T * C * K, "bytes": a2 * (T * C * s + K * C * s + T * K * 4)},
         "output_transform": {"bytes": a2 * T * K * 4 + wl.N * wl.H * wl.W * K * s},
         # fused: V and U in, y out, no M
@@ -97,10 +97,9 @@ def make_stages(plan, xd, wd, y, N_, H, W, C, K, stream):
     sh = ctypes.c_void_p(stream.cuda_stream)
     # the closures keep U, V, M and the tensor descriptors alive
     stages = {
-        "kernel_transform": lambda: lib.winograd_kernel_transform(plan._h, ctypes.byref(wt),
-                                                                  ctypes.c_void_p(U.data_ptr()), sh),
-        "input_transform": lambda: lib.winograd_input_transform(plan._h, ctypes.byref(xt),
-                                                                ctypes.c_void_p(V.data_ptr()), sh),
+        "kernel_input_transform": lambda: lib.winograd_kernel_input_transform(
+            plan._h, ctypes.byref(wt), ctypes.byref(xt), ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(V.data_ptr()),
+            sh),
     }
     if fused:
         stages["contract_output"] = lambda: lib.winograd_contract_output(

@@ -194,6 +194,12 @@ wg_status winograd_kernel_transform(wg_plan plan, const wg_tensor* w, void* U, h
  * top-left input pixel is (ty*m - 1, tx*m - 1); pixels outside x read 0. */
 wg_status winograd_input_transform(wg_plan plan, const wg_tensor* x, void* V, hipStream_t stream);
 
+/* Both transforms above in one launch (the first kernel of winograd_conv2d):
+ * U from w ([K][3][3][C]) and V from x ([N][H][W][C], same C), with the same
+ * values as the two separate calls. */
+wg_status winograd_kernel_input_transform(wg_plan plan, const wg_tensor* w, const wg_tensor* x, void* U, void* V,
+                                          hipStream_t stream);
+
 /* M[xi][t][k] = sum_c V[xi][t][c] U[xi][k][c]: alpha'^2 GEMMs [T x C][C x K]
  * on the matrix cores with fp32 accumulation (the Hadamard product of eq. (2)
  * summed over input channels). */

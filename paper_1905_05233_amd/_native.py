@@ -82,6 +82,8 @@ def lib():
                                            ctypes.POINTER(WgTensor), P]),
         "winograd_kernel_transform": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), P, P]),
         "winograd_input_transform": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), P, P]),
+        "winograd_kernel_input_transform": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),
+                                                           P, P, P]),
         "winograd_contract": (ctypes.c_int, [P, P, P, P, i64, i64, i64, P]),
         "winograd_output_transform": (ctypes.c_int, [P, P, ctypes.POINTER(WgTensor), P]),
         "winograd_contract_output": (ctypes.c_int, [P, P, P, i64, ctypes.POINTER(WgTensor), P]),

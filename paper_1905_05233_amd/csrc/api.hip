@@ -166,6 +166,14 @@ hipError_t launch_kt(int dt, const wg::Geometry& g, const wg::KernelTable& t, co
         default: return wg::launch_kernel_transform_t<2>(g, t, w, U, s);
     }
 }
+hipError_t launch_kit(int dt, const wg::Geometry& g, const wg::KernelTable& kt, const wg::InputTable& it,
+                      const void* w, const void* x, void* U, void* V, hipStream_t s) {
+    switch (dt) {
+        case 0: return wg::launch_kernel_input_transform_t<0>(g, kt, it, w, x, U, V, s);
+        case 1: return wg::launch_kernel_input_transform_t<1>(g, kt, it, w, x, U, V, s);
+        default: return wg::launch_kernel_input_transform_t<2>(g, kt, it, w, x, U, V, s);
+    }
+}
 hipError_t launch_it(int dt, const wg::Geometry& g, const wg::InputTable& t, const void* x, void* V,
                      hipStream_t s) {
     switch (dt) {
@@ -374,8 +382,9 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
     void* V = base + L.v_off;
     auto* M = reinterpret_cast<float*>(base + L.m_off);
     const int dt = plan->dtype;
-    if ((s = from_hip(launch_kt(dt, L.g, plan->ktab, w->data, U, stream), "kernel transform")) != WG_OK) return s;
-    if ((s = from_hip(launch_it(dt, L.g, plan->itab, x->data, V, stream), "input transform")) != WG_OK) return s;
+    s = from_hip(launch_kit(dt, L.g, plan->ktab, plan->itab, w->data, x->data, U, V, stream),
+                 "kernel and input transforms");
+    if (s != WG_OK) return s;
     if (L.path == WG_PATH_FUSED)
         return from_hip(launch_co(dt, L.g, plan->otab, V, U, y->data, stream), "fused contraction");
     if ((s = from_hip(launch_ct(dt, L.g, V, U, M, stream), "contraction")) != WG_OK) return s;
@@ -401,6 +410,20 @@ wg_status winograd_input_transform(wg_plan plan, const wg_tensor* x, void* V, hi
     if (!dims_ok(x->n, x->h, x->w, x->c, 1)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
     const wg::Geometry g = wg::make_geometry(x->n, x->h, x->w, x->c, 1, plan->tr.m, plan->tr.alpha);
     return from_hip(launch_it(plan->dtype, g, plan->itab, x->data, V, stream), "input transform");
+}
+
+wg_status winograd_kernel_input_transform(wg_plan plan, const wg_tensor* w, const wg_tensor* x, void* U, void* V,
+                                          hipStream_t stream) {
+    wg_status s = check_plan(plan);
+    if (s != WG_OK) return s;
+    if ((s = check_tensor(w, "w")) != WG_OK || (s = check_tensor(x, "x")) != WG_OK) return s;
+    if (!U || !V || !aligned16(U) || !aligned16(V))
+        return fail(WG_ERR_ARG, "U and V must be 16-byte aligned device pointers");
+    if (w->h != 3 || w->w != 3 || w->c != x->c) return fail(WG_ERR_ARG, "w must be [K][3][3][C] with the input's C");
+    if (!dims_ok(x->n, x->h, x->w, x->c, w->n)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
+    const wg::Geometry g = wg::make_geometry(x->n, x->h, x->w, x->c, w->n, plan->tr.m, plan->tr.alpha);
+    return from_hip(launch_kit(plan->dtype, g, plan->ktab, plan->itab, w->data, x->data, U, V, stream),
+                    "kernel and input transforms");
 }
 
 wg_status winograd_contract(wg_plan plan, const void* V, const void* U, float* M, int64_t T, int64_t C,

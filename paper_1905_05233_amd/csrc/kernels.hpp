@@ -68,6 +68,10 @@ hipError_t launch_kernel_transform_t(const Geometry& g, const KernelTable& tab, 
 template <int D>
 hipError_t launch_input_transform_t(const Geometry& g, const InputTable& tab, const void* x, void* V,
                                     hipStream_t stream);
+// Both transforms in one launch (they are independent): U from w and V from x.
+template <int D>
+hipError_t launch_kernel_input_transform_t(const Geometry& g, const KernelTable& ktab, const InputTable& itab,
+                                           const void* w, const void* x, void* U, void* V, hipStream_t stream);
 template <int D>
 hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, const float* M, void* y,
                                      hipStream_t stream);

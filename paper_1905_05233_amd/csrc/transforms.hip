@@ -34,17 +34,22 @@ constexpr int kBlock = 256;
 
 // ----------------------------------------------------------------- kernel
 // U[xi = a*alpha + b][k][c] = sum_j (sum_i G[a][i] g[i][j]) G[b][j]; one thread
-// per (row a, k, 16-byte run of channels), runs fastest, so loads and stores
-// are 16 bytes per lane.  kWhole: C is a multiple of the run, so the runs of
-// w are 16-byte aligned; otherwise w is read element by element.
-template <typename Elem, int ALPHA, bool kWhole>
-__global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, const Elem* __restrict__ w,
-                                                           Elem* __restrict__ U, int64_t K, int64_t C,
-                                                           int64_t Cp) {
+// per (row a, k, run of kRun channels), runs fastest, so loads and stores are
+// kRun elements per lane (16 bytes in the stand-alone kernel; 4 channels when
+// it shares a launch with the input transform, to keep that kernel's register
+// count low).  kWhole: C is a multiple of the run, so the runs of w are
+// aligned; otherwise w is read element by element.
+template <int BYTES> struct RunBits;
+template <> struct RunBits<16> { using type = uint4; };
+template <> struct RunBits<8> { using type = uint2; };
+
+template <typename Elem, int ALPHA, int kRun, bool kWhole>
+__device__ __forceinline__ void kernel_transform_run(const KernelTable& tab, const Elem* __restrict__ w,
+                                                     Elem* __restrict__ U, int64_t K, int64_t C, int64_t Cp,
+                                                     int64_t gid) {
     using S = Storage<Elem>;
-    constexpr int kRun = 16 / static_cast<int>(sizeof(Elem));   // channels per thread
+    using Bits = typename RunBits<kRun * sizeof(Elem)>::type;
     const int64_t runs = Cp / kRun;                              // Cp is a multiple of 8
-    const int64_t gid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     if (gid >= ALPHA * K * runs) return;
     const int64_t c = (gid % runs) * kRun;
     const int64_t k = (gid / runs) % K;
@@ -59,7 +64,7 @@ __global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, cons
             Elem e[kRun];
             if constexpr (kWhole) {
                 // a run starts inside C only if it ends inside it (for fp32, Cp may exceed C by a run)
-                *reinterpret_cast<uint4*>(e) = c < C ? *reinterpret_cast<const uint4*>(src) : uint4{0u, 0u, 0u, 0u};
+                *reinterpret_cast<Bits*>(e) = c < C ? *reinterpret_cast<const Bits*>(src) : Bits{};
             } else {
 #pragma unroll
                 for (int q = 0; q < kRun; ++q) e[q] = c + q < C ? src[q] : S::from_f32(0.0f);
@@ -88,8 +93,16 @@ __global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, cons
             for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(Gg[j][q], tab.g[b * 3 + j], acc);
             e[q] = S::from_f32(acc);   // channels past C: g = 0, so zeros
         }
-        *reinterpret_cast<uint4*>(out + b * plane) = *reinterpret_cast<const uint4*>(e);
+        *reinterpret_cast<Bits*>(out + b * plane) = *reinterpret_cast<const Bits*>(e);
     }
+}
+
+template <typename Elem, int ALPHA, bool kWhole>
+__global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, const Elem* __restrict__ w,
+                                                           Elem* __restrict__ U, int64_t K, int64_t C,
+                                                           int64_t Cp) {
+    kernel_transform_run<Elem, ALPHA, 16 / sizeof(Elem), kWhole>(tab, w, U, K, C, Cp,
+                                                                 static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x);
 }
 
 // ------------------------------------------------------------------ input
@@ -164,8 +177,9 @@ __device__ __forceinline__ void input_row_groups(int g, const InputTable& tab, c
 // kWhole: C is a multiple of the 16-byte chunk width, so a chunk lies wholly
 // inside or wholly past C; otherwise the window is fetched element by element.
 template <typename Elem, int TT, int ALPHA, bool kWhole>
-__global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input_transform(
-    InputTable tab, const Elem* __restrict__ x, Elem* __restrict__ V, Geometry geo) {
+__device__ __forceinline__ void input_transform_unit(const InputTable& tab, const Elem* __restrict__ x,
+                                                     Elem* __restrict__ V, const Geometry& geo, int64_t bid,
+                                                     int64_t G) {
     using S = Storage<Elem>;
     using P = InputShape<Elem, TT, ALPHA>;
     __shared__ __attribute__((aligned(16))) float win[TT * TT * kInCh];   // [u][v][64] fp32
@@ -174,8 +188,6 @@ __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input
     // XCD-aware numbering: the hardware deals workgroup ids round-robin to the
     // 8 XCDs; giving each XCD a contiguous run of units keeps neighbouring
     // tiles, whose windows overlap, in the same L2
-    const int64_t G = gridDim.x;
-    const int64_t bid = blockIdx.x;
     const int64_t unit = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
     const int64_t tile = unit / nch;
     const int64_t c0 = (unit % nch) * kInCh;
@@ -224,6 +236,29 @@ __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input
     // channels C..Cp-1 read as zero and so store zeros
     input_row_groups<Elem, TT, ALPHA, P::kR>(g, tab, win + c, V + tile * geo.Cp + cg, geo.T * geo.Cp,
                                              std::make_integer_sequence<int, P::kG>{});
+}
+
+template <typename Elem, int TT, int ALPHA, bool kWhole>
+__global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input_transform(
+    InputTable tab, const Elem* __restrict__ x, Elem* __restrict__ V, Geometry geo) {
+    input_transform_unit<Elem, TT, ALPHA, kWhole>(tab, x, V, geo, blockIdx.x, gridDim.x);
+}
+
+// The kernel and input transforms are independent: conv2d runs them as one
+// launch.  The first n_kt workgroups each take P::kThreads runs of the kernel
+// transform, the rest are input-transform units (one launch instead of two,
+// and the short kernel transform overlaps the input transform).
+template <typename Elem, int TT, int ALPHA, bool kWhole>
+__global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void kernel_input_transform(
+    KernelTable ktab, InputTable itab, const Elem* __restrict__ w, const Elem* __restrict__ x,
+    Elem* __restrict__ U, Elem* __restrict__ V, Geometry geo, int64_t n_kt) {
+    using P = InputShape<Elem, TT, ALPHA>;
+    const int64_t bid = blockIdx.x;
+    if (bid < n_kt) {
+        kernel_transform_run<Elem, ALPHA, 4, kWhole>(ktab, w, U, geo.K, geo.C, geo.Cp, bid * P::kThreads + threadIdx.x);
+        return;
+    }
+    input_transform_unit<Elem, TT, ALPHA, kWhole>(itab, x, V, geo, bid - n_kt, gridDim.x - n_kt);
 }
 
 // ----------------------------------------------------------------- output
@@ -375,6 +410,42 @@ hipError_t launch_input_transform_t(const Geometry& g, const InputTable& tab, co
 }
 
 template <int D>
+hipError_t launch_kernel_input_transform_t(const Geometry& g, const KernelTable& ktab, const InputTable& itab,
+                                           const void* w, const void* x, void* U, void* V, hipStream_t stream) {
+    using Elem = typename DTypeOf<D>::type;
+    const auto* wp = static_cast<const Elem*>(w);
+    const auto* xp = static_cast<const Elem*>(x);
+    auto* up = static_cast<Elem*>(U);
+    auto* vp = static_cast<Elem*>(V);
+    constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
+    const bool whole = g.C % kChunkElems == 0;   // then C is also a multiple of the 4-channel runs
+    const int64_t units = g.T * ((g.Cp + kInCh - 1) / kInCh);
+    const int64_t kt_runs = static_cast<int64_t>(g.alpha) * g.K * (g.Cp / 4);
+    if (g.t > 8) {   // larger tiles: two launches (their input transform has no registers to spare)
+        const hipError_t e = launch_kernel_transform_t<D>(g, ktab, w, U, stream);
+        return e != hipSuccess ? e : launch_input_transform_t<D>(g, itab, x, V, stream);
+    }
+#define WG_KIT_CASE(TT, A)                                                                                 \
+    if constexpr (TT <= 8) if (g.t == TT && g.alpha == A) {                                                \
+        constexpr int kThr = InputShape<Elem, TT, A>::kThreads;                                            \
+        /* a multiple of 8, so the input transform's ids keep their XCD (id mod 8) */                   \
+        const int64_t n_kt = (kt_runs + 8 * kThr - 1) / (8 * kThr) * 8;                                    \
+        if (n_kt + units > 0x7fffffff) return hipErrorInvalidValue;                                        \
+        const dim3 grid(static_cast<unsigned>(n_kt + units));                                              \
+        if (whole)                                                                                         \
+            hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, true>), grid, dim3(kThr), 0, stream, ktab, \
+                               itab, wp, xp, up, vp, g, n_kt);                                             \
+        else                                                                                               \
+            hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, false>), grid, dim3(kThr), 0, stream, ktab, \
+                               itab, wp, xp, up, vp, g, n_kt);                                             \
+        return hipGetLastError();                                                                          \
+    }
+    WG_TRANSFORM_SHAPES(WG_KIT_CASE)
+#undef WG_KIT_CASE
+    return hipErrorInvalidValue;
+}
+
+template <int D>
 hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, const float* M, void* y,
                                      hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
@@ -397,6 +468,9 @@ template hipError_t launch_kernel_transform_t<WG_DTYPE>(const Geometry&, const K
                                                         hipStream_t);
 template hipError_t launch_input_transform_t<WG_DTYPE>(const Geometry&, const InputTable&, const void*, void*,
                                                        hipStream_t);
+template hipError_t launch_kernel_input_transform_t<WG_DTYPE>(const Geometry&, const KernelTable&,
+                                                              const InputTable&, const void*, const void*, void*,
+                                                              void*, hipStream_t);
 template hipError_t launch_output_transform_t<WG_DTYPE>(const Geometry&, const OutputTable&, const float*, void*,
                                                         hipStream_t);
 

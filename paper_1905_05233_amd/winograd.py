@@ -212,6 +212,22 @@ class Plan:
                                                    _stream_handle(stream)))
         return V
 
+    def kernel_input_transform(self, w, x, stream=None):
+        """Both transforms in one launch (conv2d's first kernel): returns (U, V)."""
+        self._check_dtype(w, "w")
+        self._check_dtype(x, "x")
+        K, _, _, C = w.shape
+        Nn, H, W, _ = x.shape
+        g = self.geometry(Nn, H, W, C, K)
+        a2 = self.alpha * self.alpha
+        U = torch.empty((a2, K, g["Cp"]), dtype=w.dtype, device=w.device)
+        V = torch.empty((a2, g["T"], g["Cp"]), dtype=x.dtype, device=x.device)
+        wt, xt = _tensor(w, "w"), _tensor(x, "x")
+        N.check(self._lib.winograd_kernel_input_transform(self._h, ctypes.byref(wt), ctypes.byref(xt),
+                                                          ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(V.data_ptr()),
+                                                          _stream_handle(stream)))
+        return U, V
+
     def contract(self, V, U, C, stream=None):
         self._check_dtype(V, "V")
         self._check_dtype(U, "U")

@@ -138,3 +138,21 @@ def test_output_transform(spec, m, dtype):
         u32, ud = 2.0 ** -24, OF.UNIT_ROUNDOFF[dtype]
         tol = 2 * ((2 * al + 2) * u32 * 1.1 * Yabs + ud * np.maximum(np.abs(ref), np.abs(y)))
         assert np.all(np.abs(y - ref) <= tol)
+
+
+@pytest.mark.parametrize("spec,m", [(WL.F2_LINEAR, 2), (WL.F4_A2P1, 4), (WL.F6_TWO_QUAD, 6),
+                                    ("0,-1,1,-1/2,2,1/2,-2,a^2+1,inf", 8)])
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("shape", [(2, 9, 7, 5, 6), (1, 30, 26, 64, 40), (1, 1, 1, 1, 1)])
+def test_kernel_input_transform_matches_separate_calls(spec, m, dtype, shape):
+    """The combined launch (conv2d's first kernel) gives U and V bit-equal to
+    the two separate stage kernels, including C not a multiple of the run."""
+    p, _ = _plan(spec, m, dtype)
+    N, H, W, C, K = shape
+    x, w = WL.draw_inputs(N, H, W, C, K, "halfnormal", seed=C + K)
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
+    U2, V2 = p.kernel_input_transform(wd, xd)
+    U1, V1 = p.kernel_transform(wd), p.input_transform(xd)
+    torch.cuda.synchronize()
+    assert torch.equal(U1, U2)
+    assert torch.equal(V1, V2)
