@@ -125,13 +125,18 @@ typedef enum { WG_FACTORS_IN_B = 0, WG_FACTORS_IN_G = 1 } wg_crt_factors;
  * may differ in the last bits because the channel sums run in another order. */
 typedef enum { WG_PATH_AUTO = 0, WG_PATH_SEPARATE = 1, WG_PATH_FUSED = 2 } wg_conv_path;
 
+/* generic_transforms = 1 keeps a plan on the transform kernels that read its
+ * coefficients at run time even when its tables equal a built-in plan's (see
+ * winograd_plan_builtin); 0 (the default) lets it use the built-in kernels. */
 typedef struct {
     wg_crt_factors factors;
     wg_conv_path path;
+    int generic_transforms;
 } wg_plan_options;
 
 /* winograd_plan_create_str with options (opts == NULL means all defaults:
- * WG_FACTORS_IN_B, WG_PATH_AUTO).  An unknown option value is WG_ERR_ARG. */
+ * WG_FACTORS_IN_B, WG_PATH_AUTO, generic_transforms 0).  An unknown option
+ * value is WG_ERR_ARG. */
 wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, int r, wg_dtype dtype,
                                   const wg_plan_options* opts, wg_plan* out);
 
@@ -140,6 +145,14 @@ void winograd_plan_destroy(wg_plan plan);
 
 /* alpha' = sum over finite moduli of (2 deg - 1), plus 1 for infinity. */
 int winograd_plan_alpha(wg_plan plan);
+
+/* The library carries input and output transform kernels with the
+ * coefficients of a few plans compiled in (the F(2x2), F(4x4) and F(6x6) sets
+ * of its workloads; the compiler drops the zero terms).  *id is the index of
+ * the built-in plan whose fp32 tables are bit-identical to this plan's, which
+ * the plan then uses, or -1.  Results equal the generic kernels' for finite
+ * data (up to the sign of zero). */
+wg_status winograd_plan_builtin(wg_plan plan, int* id);
 
 /* m, r, alpha', input tile m + r - 1 and dtype of a plan. */
 wg_status winograd_plan_info(wg_plan plan, int* m, int* r, int* alpha, int* tile_in, int* dtype);

@@ -27,7 +27,7 @@ class WgPolySet(ctypes.Structure):
 
 
 class WgPlanOptions(ctypes.Structure):
-    _fields_ = [("factors", ctypes.c_int), ("path", ctypes.c_int)]
+    _fields_ = [("factors", ctypes.c_int), ("path", ctypes.c_int), ("generic_transforms", ctypes.c_int)]
 
 
 FACTOR_CODES = {"B": 0, "G": 1}
@@ -71,6 +71,7 @@ def lib():
                                                    ctypes.c_int, ctypes.POINTER(WgPlanOptions), plan_p]),
         "winograd_plan_destroy": (None, [P]),
         "winograd_plan_alpha": (ctypes.c_int, [P]),
+        "winograd_plan_builtin": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_int)]),
         "winograd_plan_info": (ctypes.c_int, [P] + [ctypes.POINTER(ctypes.c_int)] * 5),
         "winograd_plan_matrix": (ctypes.c_int, [P, ctypes.c_char, ctypes.POINTER(WgRational), sz]),
         "winograd_plan_matrix_f32": (ctypes.c_int, [P, ctypes.c_char, ctypes.POINTER(ctypes.c_float), sz]),

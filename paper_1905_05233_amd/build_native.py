@@ -20,7 +20,8 @@ LIB = os.path.join(PKG, "libwinograd_crt.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}"]
+GEN = os.path.join(BUILD, "gen")   # generated headers (builtin_plans.hpp)
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}", f"-I{GEN}"]
 # device code: no packed-fp32 instructions (v_pk_*_f32) anywhere
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-ffp-contract=fast"]
@@ -68,10 +69,21 @@ def compile_unit(unit, incremental=False):
     return _run(cmd)
 
 
+def generate_builtin_plans():
+    """Build and run the host program that writes builtin_plans.hpp (the fp32
+    tables of the built-in plans, from the library's own plan builder)."""
+    os.makedirs(GEN, exist_ok=True)
+    exe = os.path.join(GEN, "gen_builtin_plans")
+    srcs = [os.path.join(CSRC, f) for f in ("gen_builtin_plans.cpp", "plan.cpp", "rational.cpp")]
+    _run(["g++", "-O2", "-std=c++17", f"-I{CSRC}", f"-I{INCLUDE}"] + srcs + ["-o", exe])
+    _run([exe, os.path.join(GEN, "builtin_plans.hpp")])
+
+
 def build(jobs=None, verbose=False, incremental=False):
     """Compile every unit (``incremental`` skips objects newer than their
     sources, for development only) and link the shared library."""
     os.makedirs(BUILD, exist_ok=True)
+    generate_builtin_plans()
     jobs = jobs or min(8, os.cpu_count() or 4)
     with ThreadPoolExecutor(max_workers=jobs) as ex:
         logs = list(ex.map(lambda u: compile_unit(u, incremental), UNITS))

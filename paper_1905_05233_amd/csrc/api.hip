@@ -11,6 +11,7 @@
 #include <string>
 #include <vector>
 
+#include "builtin_plans.hpp"
 #include "kernels.hpp"
 #include "plan.hpp"
 #include "winograd_crt.h"
@@ -19,6 +20,7 @@ struct wg_plan_s {
     wg::Transforms tr;
     int dtype = 0;
     int path = WG_PATH_AUTO;
+    int builtin = -1;   // id of the built-in plan with the same fp32 tables, or -1
     void* ws = nullptr;
     size_t ws_bytes = 0;
     wg::InputTable itab{};
@@ -57,6 +59,28 @@ wg_status guarded(F&& f) {
     }
 }
 
+// The built-in plan whose fp32 tables (and shape) equal the plan's, or -1.
+template <class P>
+bool same_tables(const wg_plan_s* p) {
+    const int al = p->tr.alpha, t = p->tr.tile_in, m = p->tr.m;
+    if (m != P::kM || t != P::kT || al != P::kAlpha) return false;
+    for (int i = 0; i < al * t; ++i)
+        if (std::memcmp(&p->itab.bt[i], &P::bt[i], sizeof(float)) != 0) return false;
+    for (int i = 0; i < al * 3; ++i)
+        if (std::memcmp(&p->ktab.g[i], &P::g[i], sizeof(float)) != 0) return false;
+    for (int i = 0; i < m * al; ++i)
+        if (std::memcmp(&p->otab.at[i], &P::at[i], sizeof(float)) != 0) return false;
+    return true;
+}
+
+int identify_builtin(const wg_plan_s* p) {
+#define WG_SAME(ID, TT, A) \
+    if (same_tables<wg::BuiltinPlan##ID>(p)) return ID;
+    WG_BUILTIN_PLANS(WG_SAME)
+#undef WG_SAME
+    return -1;
+}
+
 wg_status finish_plan(wg::Transforms&& tr, wg_dtype dtype, wg_plan* out) {
     if (tr.alpha > wg::kMaxAlpha || tr.tile_in > wg::kMaxTile)
         return fail(WG_ERR_UNSUPPORTED, "alpha' and the input tile must be at most 16");
@@ -71,6 +95,7 @@ wg_status finish_plan(wg::Transforms&& tr, wg_dtype dtype, wg_plan* out) {
         for (int i = 0; i < 3; ++i) p->ktab.g[a * 3 + i] = p->tr.Gf[static_cast<size_t>(a * 3 + i)];
     for (int o = 0; o < m; ++o)
         for (int a = 0; a < al; ++a) p->otab.at[o * al + a] = p->tr.Af[static_cast<size_t>(a * m + o)];
+    p->builtin = identify_builtin(p);
     *out = p;
     return WG_OK;
 }
@@ -167,19 +192,19 @@ hipError_t launch_kt(int dt, const wg::Geometry& g, const wg::KernelTable& t, co
     }
 }
 hipError_t launch_kit(int dt, const wg::Geometry& g, const wg::KernelTable& kt, const wg::InputTable& it,
-                      const void* w, const void* x, void* U, void* V, hipStream_t s) {
+                      const void* w, const void* x, void* U, void* V, int bi, hipStream_t s) {
     switch (dt) {
-        case 0: return wg::launch_kernel_input_transform_t<0>(g, kt, it, w, x, U, V, s);
-        case 1: return wg::launch_kernel_input_transform_t<1>(g, kt, it, w, x, U, V, s);
-        default: return wg::launch_kernel_input_transform_t<2>(g, kt, it, w, x, U, V, s);
+        case 0: return wg::launch_kernel_input_transform_t<0>(g, kt, it, w, x, U, V, bi, s);
+        case 1: return wg::launch_kernel_input_transform_t<1>(g, kt, it, w, x, U, V, bi, s);
+        default: return wg::launch_kernel_input_transform_t<2>(g, kt, it, w, x, U, V, bi, s);
     }
 }
-hipError_t launch_it(int dt, const wg::Geometry& g, const wg::InputTable& t, const void* x, void* V,
+hipError_t launch_it(int dt, const wg::Geometry& g, const wg::InputTable& t, const void* x, void* V, int bi,
                      hipStream_t s) {
     switch (dt) {
-        case 0: return wg::launch_input_transform_t<0>(g, t, x, V, s);
-        case 1: return wg::launch_input_transform_t<1>(g, t, x, V, s);
-        default: return wg::launch_input_transform_t<2>(g, t, x, V, s);
+        case 0: return wg::launch_input_transform_t<0>(g, t, x, V, bi, s);
+        case 1: return wg::launch_input_transform_t<1>(g, t, x, V, bi, s);
+        default: return wg::launch_input_transform_t<2>(g, t, x, V, bi, s);
     }
 }
 hipError_t launch_ct(int dt, const wg::Geometry& g, const void* V, const void* U, float* M, hipStream_t s) {
@@ -189,12 +214,12 @@ hipError_t launch_ct(int dt, const wg::Geometry& g, const void* V, const void* U
         default: return wg::launch_contract_t<2>(g, V, U, M, s);
     }
 }
-hipError_t launch_ot(int dt, const wg::Geometry& g, const wg::OutputTable& t, const float* M, void* y,
+hipError_t launch_ot(int dt, const wg::Geometry& g, const wg::OutputTable& t, const float* M, void* y, int bi,
                      hipStream_t s) {
     switch (dt) {
-        case 0: return wg::launch_output_transform_t<0>(g, t, M, y, s);
-        case 1: return wg::launch_output_transform_t<1>(g, t, M, y, s);
-        default: return wg::launch_output_transform_t<2>(g, t, M, y, s);
+        case 0: return wg::launch_output_transform_t<0>(g, t, M, y, bi, s);
+        case 1: return wg::launch_output_transform_t<1>(g, t, M, y, bi, s);
+        default: return wg::launch_output_transform_t<2>(g, t, M, y, bi, s);
     }
 }
 hipError_t launch_co(int dt, const wg::Geometry& g, const wg::OutputTable& t, const void* V, const void* U,
@@ -276,13 +301,18 @@ wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, 
         const int path = opts ? static_cast<int>(opts->path) : WG_PATH_AUTO;
         if (path != WG_PATH_AUTO && path != WG_PATH_SEPARATE && path != WG_PATH_FUSED)
             return fail(WG_ERR_ARG, "unknown convolution path");
+        const int generic = opts ? opts->generic_transforms : 0;
+        if (generic != 0 && generic != 1) return fail(WG_ERR_ARG, "generic_transforms must be 0 or 1");
         const std::vector<wg::Modulus> mods = wg::parse_moduli(moduli);
         std::vector<wg::Rat> pts;
         bool inf = true;
         if (inner && inner[0] != '\0') wg::parse_points(inner, &pts, &inf);
         else pts = {wg::Rat(0), wg::Rat(-1)};
         s = finish_plan(wg::build_transforms(mods, pts, inf, m, r, factors == WG_FACTORS_IN_G), dtype, out);
-        if (s == WG_OK) (*out)->path = path;
+        if (s == WG_OK) {
+            (*out)->path = path;
+            if (generic) (*out)->builtin = -1;
+        }
         return s;
     });
 }
@@ -290,6 +320,12 @@ wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, 
 void winograd_plan_destroy(wg_plan plan) { delete plan; }
 
 int winograd_plan_alpha(wg_plan plan) { return plan ? plan->tr.alpha : 0; }
+
+wg_status winograd_plan_builtin(wg_plan plan, int* id) {
+    if (!plan || !id) return fail(WG_ERR_ARG, "null argument");
+    *id = plan->builtin;
+    return WG_OK;
+}
 
 wg_status winograd_plan_info(wg_plan plan, int* m, int* r, int* alpha, int* tile_in, int* dtype) {
     if (!plan) return fail(WG_ERR_ARG, "null plan");
@@ -382,13 +418,13 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
     void* V = base + L.v_off;
     auto* M = reinterpret_cast<float*>(base + L.m_off);
     const int dt = plan->dtype;
-    s = from_hip(launch_kit(dt, L.g, plan->ktab, plan->itab, w->data, x->data, U, V, stream),
+    s = from_hip(launch_kit(dt, L.g, plan->ktab, plan->itab, w->data, x->data, U, V, plan->builtin, stream),
                  "kernel and input transforms");
     if (s != WG_OK) return s;
     if (L.path == WG_PATH_FUSED)
         return from_hip(launch_co(dt, L.g, plan->otab, V, U, y->data, stream), "fused contraction");
     if ((s = from_hip(launch_ct(dt, L.g, V, U, M, stream), "contraction")) != WG_OK) return s;
-    return from_hip(launch_ot(dt, L.g, plan->otab, M, y->data, stream), "output transform");
+    return from_hip(launch_ot(dt, L.g, plan->otab, M, y->data, plan->builtin, stream), "output transform");
 }
 
 wg_status winograd_kernel_transform(wg_plan plan, const wg_tensor* w, void* U, hipStream_t stream) {
@@ -409,7 +445,7 @@ wg_status winograd_input_transform(wg_plan plan, const wg_tensor* x, void* V, hi
     if (!V || !aligned16(V)) return fail(WG_ERR_ARG, "V must be a 16-byte aligned device pointer");
     if (!dims_ok(x->n, x->h, x->w, x->c, 1)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
     const wg::Geometry g = wg::make_geometry(x->n, x->h, x->w, x->c, 1, plan->tr.m, plan->tr.alpha);
-    return from_hip(launch_it(plan->dtype, g, plan->itab, x->data, V, stream), "input transform");
+    return from_hip(launch_it(plan->dtype, g, plan->itab, x->data, V, plan->builtin, stream), "input transform");
 }
 
 wg_status winograd_kernel_input_transform(wg_plan plan, const wg_tensor* w, const wg_tensor* x, void* U, void* V,
@@ -422,7 +458,7 @@ wg_status winograd_kernel_input_transform(wg_plan plan, const wg_tensor* w, cons
     if (w->h != 3 || w->w != 3 || w->c != x->c) return fail(WG_ERR_ARG, "w must be [K][3][3][C] with the input's C");
     if (!dims_ok(x->n, x->h, x->w, x->c, w->n)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
     const wg::Geometry g = wg::make_geometry(x->n, x->h, x->w, x->c, w->n, plan->tr.m, plan->tr.alpha);
-    return from_hip(launch_kit(plan->dtype, g, plan->ktab, plan->itab, w->data, x->data, U, V, stream),
+    return from_hip(launch_kit(plan->dtype, g, plan->ktab, plan->itab, w->data, x->data, U, V, plan->builtin, stream),
                     "kernel and input transforms");
 }
 
@@ -445,7 +481,7 @@ wg_status winograd_output_transform(wg_plan plan, const float* M, wg_tensor* y, 
     if (!M || !aligned16(M)) return fail(WG_ERR_ARG, "M must be a 16-byte aligned device pointer");
     if (!dims_ok(y->n, y->h, y->w, 1, y->c)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
     const wg::Geometry g = wg::make_geometry(y->n, y->h, y->w, 1, y->c, plan->tr.m, plan->tr.alpha);
-    return from_hip(launch_ot(plan->dtype, g, plan->otab, M, y->data, stream), "output transform");
+    return from_hip(launch_ot(plan->dtype, g, plan->otab, M, y->data, plan->builtin, stream), "output transform");
 }
 
 wg_status winograd_contract_output(wg_plan plan, const void* V, const void* U, int64_t C, wg_tensor* y,

@@ -19,8 +19,14 @@ template <> struct Storage<float> {
 
 template <> struct Storage<_Float16> {
     static __device__ __forceinline__ float to_f32(_Float16 v) { return static_cast<float>(v); }
-    // IEEE conversion, round to nearest even (the default rounding mode)
-    static __device__ __forceinline__ _Float16 from_f32(float f) { return static_cast<_Float16>(f); }
+    // IEEE conversion, round to nearest even (the default rounding mode), of
+    // the value as rounded to fp32.  The empty asm keeps the compiler from
+    // folding a preceding fp32 fma into the conversion (v_fma_mix*_f16, one
+    // rounding straight to fp16), which would skip the fp32 rounding.
+    static __device__ __forceinline__ _Float16 from_f32(float f) {
+        asm("" : "+v"(f));
+        return static_cast<_Float16>(f);
+    }
 };
 
 template <> struct Storage<bf16_t> {

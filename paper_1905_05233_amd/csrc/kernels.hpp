@@ -65,16 +65,19 @@ inline bool transform_shape_supported(int t, int alpha) {
 template <int D>
 hipError_t launch_kernel_transform_t(const Geometry& g, const KernelTable& tab, const void* w, void* U,
                                      hipStream_t stream);
+// builtin: the id of a built-in plan whose tables the plan has (its
+// constant-coefficient kernels are used), or -1.
 template <int D>
-hipError_t launch_input_transform_t(const Geometry& g, const InputTable& tab, const void* x, void* V,
+hipError_t launch_input_transform_t(const Geometry& g, const InputTable& tab, const void* x, void* V, int builtin,
                                     hipStream_t stream);
 // Both transforms in one launch (they are independent): U from w and V from x.
 template <int D>
 hipError_t launch_kernel_input_transform_t(const Geometry& g, const KernelTable& ktab, const InputTable& itab,
-                                           const void* w, const void* x, void* U, void* V, hipStream_t stream);
+                                           const void* w, const void* x, void* U, void* V, int builtin,
+                                           hipStream_t stream);
 template <int D>
 hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, const float* M, void* y,
-                                     hipStream_t stream);
+                                     int builtin, hipStream_t stream);
 template <int D>
 hipError_t launch_contract_t(const Geometry& g, const void* V, const void* U, float* M, hipStream_t stream);
 

@@ -19,6 +19,7 @@
 // register arrays have compile-time sizes.
 #include <utility>
 
+#include "builtin_plans.hpp"
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -31,6 +32,27 @@ namespace wg {
 namespace {
 
 constexpr int kBlock = 256;
+
+// Transform coefficients of the input and output transforms: read from the
+// kernel-argument tables (any plan) or, for the built-in plans, compile-time
+// constants, with which the compiler drops every term whose coefficient is
+// zero.  Dropping a zero term leaves the sum unchanged for finite data (up to
+// the sign of a zero result).
+struct RuntimeCoefs {
+    static constexpr bool kConst = false;
+    static __device__ __forceinline__ float bt(const InputTable& t, int i) { return t.bt[i]; }
+    static __device__ __forceinline__ float at(const OutputTable& t, int i) { return t.at[i]; }
+};
+template <class P> struct ConstCoefs {
+    static constexpr bool kConst = true;
+    static __device__ __forceinline__ constexpr float bt(const InputTable&, int i) { return P::bt[i]; }
+    static __device__ __forceinline__ constexpr float at(const OutputTable&, int i) { return P::at[i]; }
+};
+// acc + c * x as one fused multiply-add; skipped for a compile-time zero c
+template <class CO> __device__ __forceinline__ float term(float c, float x, float acc) {
+    if (CO::kConst && c == 0.0f) return acc;
+    return __builtin_fmaf(c, x, acc);
+}
 
 // ----------------------------------------------------------------- kernel
 // U[xi = a*alpha + b][k][c] = sum_j (sum_i G[a][i] g[i][j]) G[b][j]; one thread
@@ -135,7 +157,7 @@ struct InputShape {
 
 // Both passes for rows A0 .. A0+R-1 of one (tile, channel): pass 1 in ascending
 // u, pass 2 in ascending v, rounded to the storage type at the store.
-template <typename Elem, int TT, int ALPHA, int R, int A0>
+template <typename Elem, int TT, int ALPHA, int R, int A0, class CO>
 __device__ __forceinline__ void input_rows(const InputTable& tab, const float* wb, Elem* __restrict__ out,
                                            int64_t plane) {
     using S = Storage<Elem>;
@@ -150,7 +172,7 @@ __device__ __forceinline__ void input_rows(const InputTable& tab, const float* w
             float acc = 0.0f;
             if (A0 + r < ALPHA) {
 #pragma unroll
-                for (int u = 0; u < TT; ++u) acc = __builtin_fmaf(tab.bt[(A0 + r) * TT + u], col[u], acc);
+                for (int u = 0; u < TT; ++u) acc = term<CO>(CO::bt(tab, (A0 + r) * TT + u), col[u], acc);
             }
             W1[r][v] = acc;
         }
@@ -162,21 +184,21 @@ __device__ __forceinline__ void input_rows(const InputTable& tab, const float* w
         for (int b = 0; b < ALPHA; ++b) {
             float acc = 0.0f;
 #pragma unroll
-            for (int v = 0; v < TT; ++v) acc = __builtin_fmaf(W1[r][v], tab.bt[b * TT + v], acc);
+            for (int v = 0; v < TT; ++v) acc = term<CO>(CO::bt(tab, b * TT + v), W1[r][v], acc);
             out[((A0 + r) * ALPHA + b) * plane] = S::from_f32(acc);
         }
     }
 }
 
-template <typename Elem, int TT, int ALPHA, int R, int... Gs>
+template <typename Elem, int TT, int ALPHA, int R, class CO, int... Gs>
 __device__ __forceinline__ void input_row_groups(int g, const InputTable& tab, const float* wb, Elem* out,
                                                  int64_t plane, std::integer_sequence<int, Gs...>) {
-    ((g == Gs ? (input_rows<Elem, TT, ALPHA, R, Gs * R>(tab, wb, out, plane), 0) : 0), ...);
+    ((g == Gs ? (input_rows<Elem, TT, ALPHA, R, Gs * R, CO>(tab, wb, out, plane), 0) : 0), ...);
 }
 
 // kWhole: C is a multiple of the 16-byte chunk width, so a chunk lies wholly
 // inside or wholly past C; otherwise the window is fetched element by element.
-template <typename Elem, int TT, int ALPHA, bool kWhole>
+template <typename Elem, int TT, int ALPHA, bool kWhole, class CO>
 __device__ __forceinline__ void input_transform_unit(const InputTable& tab, const Elem* __restrict__ x,
                                                      Elem* __restrict__ V, const Geometry& geo, int64_t bid,
                                                      int64_t G) {
@@ -234,21 +256,21 @@ __device__ __forceinline__ void input_transform_unit(const InputTable& tab, cons
     const int64_t cg = c0 + c;
     if (cg >= geo.Cp) return;
     // channels C..Cp-1 read as zero and so store zeros
-    input_row_groups<Elem, TT, ALPHA, P::kR>(g, tab, win + c, V + tile * geo.Cp + cg, geo.T * geo.Cp,
-                                             std::make_integer_sequence<int, P::kG>{});
+    input_row_groups<Elem, TT, ALPHA, P::kR, CO>(g, tab, win + c, V + tile * geo.Cp + cg, geo.T * geo.Cp,
+                                                 std::make_integer_sequence<int, P::kG>{});
 }
 
-template <typename Elem, int TT, int ALPHA, bool kWhole>
+template <typename Elem, int TT, int ALPHA, bool kWhole, class CO>
 __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input_transform(
     InputTable tab, const Elem* __restrict__ x, Elem* __restrict__ V, Geometry geo) {
-    input_transform_unit<Elem, TT, ALPHA, kWhole>(tab, x, V, geo, blockIdx.x, gridDim.x);
+    input_transform_unit<Elem, TT, ALPHA, kWhole, CO>(tab, x, V, geo, blockIdx.x, gridDim.x);
 }
 
 // The kernel and input transforms are independent: conv2d runs them as one
 // launch.  The first n_kt workgroups each take P::kThreads runs of the kernel
 // transform, the rest are input-transform units (one launch instead of two,
 // and the short kernel transform overlaps the input transform).
-template <typename Elem, int TT, int ALPHA, bool kWhole>
+template <typename Elem, int TT, int ALPHA, bool kWhole, class CO>
 __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void kernel_input_transform(
     KernelTable ktab, InputTable itab, const Elem* __restrict__ w, const Elem* __restrict__ x,
     Elem* __restrict__ U, Elem* __restrict__ V, Geometry geo, int64_t n_kt) {
@@ -258,7 +280,7 @@ __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void kerne
         kernel_transform_run<Elem, ALPHA, 4, kWhole>(ktab, w, U, geo.K, geo.C, geo.Cp, bid * P::kThreads + threadIdx.x);
         return;
     }
-    input_transform_unit<Elem, TT, ALPHA, kWhole>(itab, x, V, geo, bid - n_kt, gridDim.x - n_kt);
+    input_transform_unit<Elem, TT, ALPHA, kWhole, CO>(itab, x, V, geo, bid - n_kt, gridDim.x - n_kt);
 }
 
 // ----------------------------------------------------------------- output
@@ -283,7 +305,7 @@ struct OutputShape {
     static constexpr int kThreads = 64 * kG;
 };
 
-template <typename Elem, int MM, int ALPHA, int O0>
+template <typename Elem, int MM, int ALPHA, int O0, class CO>
 __device__ __forceinline__ void output_rows(const OutputTable& tab, const float* __restrict__ in, int64_t plane,
                                             Elem* __restrict__ yk, int64_t hr0, int64_t wc0, const Geometry& geo) {
     using S = Storage<Elem>;
@@ -302,7 +324,7 @@ __device__ __forceinline__ void output_rows(const OutputTable& tab, const float*
             float acc = 0.0f;
             if (O0 + r < MM) {
 #pragma unroll
-                for (int a = 0; a < ALPHA; ++a) acc = __builtin_fmaf(tab.at[(O0 + r) * ALPHA + a], Mv[a][b], acc);
+                for (int a = 0; a < ALPHA; ++a) acc = term<CO>(CO::at(tab, (O0 + r) * ALPHA + a), Mv[a][b], acc);
             }
             Z[r][b] = acc;
         }
@@ -316,23 +338,23 @@ __device__ __forceinline__ void output_rows(const OutputTable& tab, const float*
             const int64_t wc = wc0 + p;
             float acc = 0.0f;
 #pragma unroll
-            for (int b = 0; b < ALPHA; ++b) acc = __builtin_fmaf(Z[r][b], tab.at[p * ALPHA + b], acc);
+            for (int b = 0; b < ALPHA; ++b) acc = term<CO>(CO::at(tab, p * ALPHA + b), Z[r][b], acc);
             if (wc < geo.W) yk[(hr * geo.W + wc) * geo.K] = S::from_f32(acc);
         }
     }
 }
 
-template <typename Elem, int MM, int ALPHA, int... Gs>
+template <typename Elem, int MM, int ALPHA, class CO, int... Gs>
 __device__ __forceinline__ void output_row_groups(int g, const OutputTable& tab, const float* in, int64_t plane,
                                                   Elem* yk, int64_t hr0, int64_t wc0, const Geometry& geo,
                                                   std::integer_sequence<int, Gs...>) {
-    ((g == Gs ? (output_rows<Elem, MM, ALPHA, Gs * OutputShape<MM, ALPHA>::kR>(tab, in, plane, yk, hr0, wc0, geo),
+    ((g == Gs ? (output_rows<Elem, MM, ALPHA, Gs * OutputShape<MM, ALPHA>::kR, CO>(tab, in, plane, yk, hr0, wc0, geo),
                  0)
               : 0),
      ...);
 }
 
-template <typename Elem, int MM, int ALPHA>
+template <typename Elem, int MM, int ALPHA, class CO>
 __global__ __launch_bounds__((OutputShape<MM, ALPHA>::kThreads)) void output_transform(
     OutputTable tab, const float* __restrict__ Mx, Elem* __restrict__ y, Geometry geo) {
     const int64_t nkc = (geo.K + kOutCh - 1) / kOutCh;
@@ -344,7 +366,7 @@ __global__ __launch_bounds__((OutputShape<MM, ALPHA>::kThreads)) void output_tra
     const int64_t tx = tile % geo.tw;
     const int64_t ty = (tile / geo.tw) % geo.th;
     const int64_t n = tile / (geo.tw * geo.th);
-    output_row_groups<Elem, MM, ALPHA>(g, tab, Mx + tile * geo.Kp + k, geo.T * geo.Kp,
+    output_row_groups<Elem, MM, ALPHA, CO>(g, tab, Mx + tile * geo.Kp + k, geo.T * geo.Kp,
                                        y + n * geo.H * geo.W * geo.K + k, ty * MM, tx * MM, geo,
                                        std::make_integer_sequence<int, OutputShape<MM, ALPHA>::kG>{});
 }
@@ -384,26 +406,69 @@ hipError_t launch_kernel_transform_t(const Geometry& g, const KernelTable& tab, 
     return hipGetLastError();
 }
 
+// One launch of each kernel shape, with the coefficient source CO.
+template <typename Elem, int TT, int A, class CO>
+hipError_t launch_it(const Geometry& g, const InputTable& tab, const Elem* xp, Elem* vp, hipStream_t stream) {
+    constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
+    const int64_t units = g.T * ((g.Cp + kInCh - 1) / kInCh);
+    if (units > 0x7fffffff) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(units)), block(InputShape<Elem, TT, A>::kThreads);
+    if (g.C % kChunkElems == 0)
+        hipLaunchKernelGGL((input_transform<Elem, TT, A, true, CO>), grid, block, 0, stream, tab, xp, vp, g);
+    else
+        hipLaunchKernelGGL((input_transform<Elem, TT, A, false, CO>), grid, block, 0, stream, tab, xp, vp, g);
+    return hipGetLastError();
+}
+
+template <typename Elem, int TT, int A, class CO>
+hipError_t launch_kit(const Geometry& g, const KernelTable& ktab, const InputTable& itab, const Elem* wp,
+                      const Elem* xp, Elem* up, Elem* vp, hipStream_t stream) {
+    constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
+    constexpr int kThr = InputShape<Elem, TT, A>::kThreads;
+    const int64_t units = g.T * ((g.Cp + kInCh - 1) / kInCh);
+    const int64_t kt_runs = static_cast<int64_t>(g.alpha) * g.K * (g.Cp / 4);
+    // a multiple of 8, so the input transform's ids keep their XCD (id mod 8)
+    const int64_t n_kt = (kt_runs + 8 * kThr - 1) / (8 * kThr) * 8;
+    if (n_kt + units > 0x7fffffff) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(n_kt + units));
+    if (g.C % kChunkElems == 0)   // then C is also a multiple of the 4-channel runs
+        hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, true, CO>), grid, dim3(kThr), 0, stream, ktab, itab,
+                           wp, xp, up, vp, g, n_kt);
+    else
+        hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, false, CO>), grid, dim3(kThr), 0, stream, ktab, itab,
+                           wp, xp, up, vp, g, n_kt);
+    return hipGetLastError();
+}
+
+template <typename Elem, int TT, int A, class CO>
+hipError_t launch_ot(const Geometry& g, const OutputTable& tab, const float* M, Elem* yp, hipStream_t stream) {
+    const int64_t units = g.T * ((g.K + kOutCh - 1) / kOutCh);
+    if (units > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((output_transform<Elem, TT - 2, A, CO>), dim3(static_cast<unsigned>(units)),
+                       dim3(OutputShape<TT - 2, A>::kThreads), 0, stream, tab, M, yp, g);
+    return hipGetLastError();
+}
+
+// Dispatch: the constant-coefficient instance of a built-in plan (builtin =
+// its id, when the shape matches), else the kernel-argument tables.
 template <int D>
 hipError_t launch_input_transform_t(const Geometry& g, const InputTable& tab, const void* x, void* V,
-                                    hipStream_t stream) {
+                                    int builtin, hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
     const auto* xp = static_cast<const Elem*>(x);
     auto* vp = static_cast<Elem*>(V);
-    constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
-    const bool whole = g.C % kChunkElems == 0;
-    const int64_t units = g.T * ((g.Cp + kInCh - 1) / kInCh);
-    if (units > 0x7fffffff) return hipErrorInvalidValue;
-    const dim3 grid(static_cast<unsigned>(units));
-#define WG_IT_CASE(TT, A)                                                                                  \
-    if (g.t == TT && g.alpha == A) {                                                                       \
-        const dim3 block(InputShape<Elem, TT, A>::kThreads);                                               \
-        if (whole)                                                                                         \
-            hipLaunchKernelGGL((input_transform<Elem, TT, A, true>), grid, block, 0, stream, tab, xp, vp, g); \
-        else                                                                                               \
-            hipLaunchKernelGGL((input_transform<Elem, TT, A, false>), grid, block, 0, stream, tab, xp, vp, g); \
-        return hipGetLastError();                                                                          \
+    switch (builtin) {
+#define WG_IT_BUILTIN(ID, TT, A)                                                                           \
+    case ID:                                                                                               \
+        if (g.t == TT && g.alpha == A) return launch_it<Elem, TT, A, ConstCoefs<BuiltinPlan##ID>>(g, tab, xp, vp, stream); \
+        break;
+        WG_BUILTIN_PLANS(WG_IT_BUILTIN)
+#undef WG_IT_BUILTIN
+        default:
+            break;
     }
+#define WG_IT_CASE(TT, A) \
+    if (g.t == TT && g.alpha == A) return launch_it<Elem, TT, A, RuntimeCoefs>(g, tab, xp, vp, stream);
     WG_TRANSFORM_SHAPES(WG_IT_CASE)
 #undef WG_IT_CASE
     return hipErrorInvalidValue;
@@ -411,35 +476,31 @@ hipError_t launch_input_transform_t(const Geometry& g, const InputTable& tab, co
 
 template <int D>
 hipError_t launch_kernel_input_transform_t(const Geometry& g, const KernelTable& ktab, const InputTable& itab,
-                                           const void* w, const void* x, void* U, void* V, hipStream_t stream) {
+                                           const void* w, const void* x, void* U, void* V, int builtin,
+                                           hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
     const auto* wp = static_cast<const Elem*>(w);
     const auto* xp = static_cast<const Elem*>(x);
     auto* up = static_cast<Elem*>(U);
     auto* vp = static_cast<Elem*>(V);
-    constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
-    const bool whole = g.C % kChunkElems == 0;   // then C is also a multiple of the 4-channel runs
-    const int64_t units = g.T * ((g.Cp + kInCh - 1) / kInCh);
-    const int64_t kt_runs = static_cast<int64_t>(g.alpha) * g.K * (g.Cp / 4);
     if (g.t > 8) {   // larger tiles: two launches (their input transform has no registers to spare)
         const hipError_t e = launch_kernel_transform_t<D>(g, ktab, w, U, stream);
-        return e != hipSuccess ? e : launch_input_transform_t<D>(g, itab, x, V, stream);
+        return e != hipSuccess ? e : launch_input_transform_t<D>(g, itab, x, V, builtin, stream);
+    }
+    switch (builtin) {
+#define WG_KIT_BUILTIN(ID, TT, A)                                                                          \
+    case ID:                                                                                               \
+        if (g.t == TT && g.alpha == A)                                                                     \
+            return launch_kit<Elem, TT, A, ConstCoefs<BuiltinPlan##ID>>(g, ktab, itab, wp, xp, up, vp, stream); \
+        break;
+        WG_BUILTIN_PLANS(WG_KIT_BUILTIN)
+#undef WG_KIT_BUILTIN
+        default:
+            break;
     }
 #define WG_KIT_CASE(TT, A)                                                                                 \
-    if constexpr (TT <= 8) if (g.t == TT && g.alpha == A) {                                                \
-        constexpr int kThr = InputShape<Elem, TT, A>::kThreads;                                            \
-        /* a multiple of 8, so the input transform's ids keep their XCD (id mod 8) */                   \
-        const int64_t n_kt = (kt_runs + 8 * kThr - 1) / (8 * kThr) * 8;                                    \
-        if (n_kt + units > 0x7fffffff) return hipErrorInvalidValue;                                        \
-        const dim3 grid(static_cast<unsigned>(n_kt + units));                                              \
-        if (whole)                                                                                         \
-            hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, true>), grid, dim3(kThr), 0, stream, ktab, \
-                               itab, wp, xp, up, vp, g, n_kt);                                             \
-        else                                                                                               \
-            hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, false>), grid, dim3(kThr), 0, stream, ktab, \
-                               itab, wp, xp, up, vp, g, n_kt);                                             \
-        return hipGetLastError();                                                                          \
-    }
+    if constexpr (TT <= 8)                                                                                 \
+        if (g.t == TT && g.alpha == A) return launch_kit<Elem, TT, A, RuntimeCoefs>(g, ktab, itab, wp, xp, up, vp, stream);
     WG_TRANSFORM_SHAPES(WG_KIT_CASE)
 #undef WG_KIT_CASE
     return hipErrorInvalidValue;
@@ -447,18 +508,21 @@ hipError_t launch_kernel_input_transform_t(const Geometry& g, const KernelTable&
 
 template <int D>
 hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, const float* M, void* y,
-                                     hipStream_t stream) {
+                                     int builtin, hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
     auto* yp = static_cast<Elem*>(y);
-    const int64_t units = g.T * ((g.K + kOutCh - 1) / kOutCh);
-    if (units > 0x7fffffff) return hipErrorInvalidValue;
-    const dim3 grid(static_cast<unsigned>(units));
-#define WG_OT_CASE(TT, A)                                                                                    \
-    if (g.t == TT && g.alpha == A) {                                                                         \
-        hipLaunchKernelGGL((output_transform<Elem, TT - 2, A>), grid, dim3(OutputShape<TT - 2, A>::kThreads), 0, \
-                           stream, tab, M, yp, g);                                                           \
-        return hipGetLastError();                                                                            \
+    switch (builtin) {
+#define WG_OT_BUILTIN(ID, TT, A)                                                                           \
+    case ID:                                                                                               \
+        if (g.t == TT && g.alpha == A) return launch_ot<Elem, TT, A, ConstCoefs<BuiltinPlan##ID>>(g, tab, M, yp, stream); \
+        break;
+        WG_BUILTIN_PLANS(WG_OT_BUILTIN)
+#undef WG_OT_BUILTIN
+        default:
+            break;
     }
+#define WG_OT_CASE(TT, A) \
+    if (g.t == TT && g.alpha == A) return launch_ot<Elem, TT, A, RuntimeCoefs>(g, tab, M, yp, stream);
     WG_TRANSFORM_SHAPES(WG_OT_CASE)
 #undef WG_OT_CASE
     return hipErrorInvalidValue;
@@ -466,12 +530,12 @@ hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, 
 
 template hipError_t launch_kernel_transform_t<WG_DTYPE>(const Geometry&, const KernelTable&, const void*, void*,
                                                         hipStream_t);
-template hipError_t launch_input_transform_t<WG_DTYPE>(const Geometry&, const InputTable&, const void*, void*,
+template hipError_t launch_input_transform_t<WG_DTYPE>(const Geometry&, const InputTable&, const void*, void*, int,
                                                        hipStream_t);
 template hipError_t launch_kernel_input_transform_t<WG_DTYPE>(const Geometry&, const KernelTable&,
                                                               const InputTable&, const void*, const void*, void*,
-                                                              void*, hipStream_t);
+                                                              void*, int, hipStream_t);
 template hipError_t launch_output_transform_t<WG_DTYPE>(const Geometry&, const OutputTable&, const float*, void*,
-                                                        hipStream_t);
+                                                        int, hipStream_t);
 
 }  // namespace wg

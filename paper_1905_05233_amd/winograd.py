@@ -37,11 +37,13 @@ def _tensor(t, name, shape=None):
 class Plan:
     """A Winograd plan F(m x m, 3 x 3) built from a modulus set (Algorithms 1, 2)."""
 
-    def __init__(self, moduli, m, dtype="f32", inner="0,-1,inf", r=3, factors="B", path="auto"):
+    def __init__(self, moduli, m, dtype="f32", inner="0,-1,inf", r=3, factors="B", path="auto",
+                 generic_transforms=False):
         """``factors``: where the CRT factors N_i go, "B" (the paper's
         matrices) or "G" (on the kernel residues).  ``path``: "separate"
         (M through memory), "fused" (contraction and output transform in one
-        kernel) or "auto" (chosen per layer shape)."""
+        kernel) or "auto" (chosen per layer shape).  ``generic_transforms``:
+        never use the built-in constant-coefficient transform kernels."""
         if dtype not in N.DTYPE_CODES:
             raise ValueError(f"dtype must be one of {list(N.DTYPE_CODES)}")
         if factors not in N.FACTOR_CODES:
@@ -50,11 +52,11 @@ class Plan:
             raise ValueError(f"path must be one of {list(N.PATH_CODES)}")
         self._lib = N.lib()
         self._h = ctypes.c_void_p()
-        if factors == "B" and path == "auto":
+        if factors == "B" and path == "auto" and not generic_transforms:
             N.check(self._lib.winograd_plan_create_str(moduli.encode(), (inner or "").encode(), int(m), int(r),
                                                        N.DTYPE_CODES[dtype], ctypes.byref(self._h)))
         else:
-            opts = N.WgPlanOptions(N.FACTOR_CODES[factors], N.PATH_CODES[path])
+            opts = N.WgPlanOptions(N.FACTOR_CODES[factors], N.PATH_CODES[path], 1 if generic_transforms else 0)
             N.check(self._lib.winograd_plan_create_ex(moduli.encode(), (inner or "").encode(), int(m), int(r),
                                                       N.DTYPE_CODES[dtype], ctypes.byref(opts),
                                                       ctypes.byref(self._h)))
@@ -112,6 +114,14 @@ class Plan:
         buf = (ctypes.c_float * (rows * cols))()
         N.check(self._lib.winograd_plan_matrix_f32(self._h, which.encode(), buf, rows * cols))
         return [[buf[i * cols + j] for j in range(cols)] for i in range(rows)]
+
+    @property
+    def builtin(self):
+        """Index of the built-in plan whose constant-coefficient transform
+        kernels this plan uses, or -1."""
+        out = ctypes.c_int()
+        N.check(self._lib.winograd_plan_builtin(self._h, ctypes.byref(out)))
+        return out.value
 
     @property
     def ratio(self):

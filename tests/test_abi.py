@@ -230,3 +230,23 @@ def test_geometry_helpers():
     g = p.geometry(16, 28, 28, 256, 256)
     assert g["T"] == 16 * 5 * 5 and g["Cp"] == 256
     assert OC.tile_counts(28, 28, 6) == (5, 5)
+
+
+def test_builtin_plans_identified():
+    """The plans of the workloads run on the constant-coefficient transform
+    kernels; any other table (other points, inner points, factor placement)
+    and the generic option keep the run-time tables."""
+    expect = [(WL.F2_LINEAR, 2), (WL.F4_LINEAR, 4), (WL.F4_A2P1, 4), (WL.F6_LINEAR, 6), (WL.F6_TWO_QUAD, 6),
+              (WL.F6_ONE_A2P1, 6)]
+    for i, (spec, m) in enumerate(expect):
+        for dt in ("f32", "bf16"):
+            assert Plan(spec, m=m, dtype=dt).builtin == i
+        assert Plan(spec, m=m, generic_transforms=True).builtin == -1
+        assert Plan(spec, m=m, factors="G").builtin == -1
+    assert Plan("0,1,-1,2,-2,inf", m=4).builtin == -1
+    assert Plan(WL.F4_A2P1, m=4, inner="0,1,inf").builtin == -1
+    assert Plan("0,a^2+1,inf", m=2).builtin == -1
+    lib = N.lib()
+    h = ctypes.c_void_p()
+    bad = N.WgPlanOptions(0, 0, 2)
+    assert lib.winograd_plan_create_ex(WL.F4_LINEAR.encode(), b"", 4, 3, 0, ctypes.byref(bad), ctypes.byref(h)) == 1

@@ -156,3 +156,29 @@ def test_kernel_input_transform_matches_separate_calls(spec, m, dtype, shape):
     torch.cuda.synchronize()
     assert torch.equal(U1, U2)
     assert torch.equal(V1, V2)
+
+
+BUILTIN = [(WL.F2_LINEAR, 2), (WL.F4_LINEAR, 4), (WL.F4_A2P1, 4), (WL.F6_LINEAR, 6), (WL.F6_TWO_QUAD, 6),
+           (WL.F6_ONE_A2P1, 6)]
+
+
+@pytest.mark.parametrize("spec,m", BUILTIN)
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_builtin_transforms_equal_generic(spec, m, dtype):
+    """Constant-coefficient transform kernels (zero terms dropped) against the
+    kernels that read the same tables at run time: V and y equal value for
+    value (finite data), on a shape with ragged tiles and channels."""
+    from paper_1905_05233_amd.winograd import Plan
+    pb, pg = Plan(spec, m=m, dtype=dtype, path="separate"), Plan(spec, m=m, dtype=dtype, path="separate",
+                                                                  generic_transforms=True)
+    assert pb.builtin >= 0 and pg.builtin == -1
+    N, H, W, C, K = 2, 23, 19, 20, 36
+    x, w = WL.draw_inputs(N, H, W, C, K, "halfnormal", seed=m + C)
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
+    Ub, Vb = pb.kernel_input_transform(wd, xd)
+    Ug, Vg = pg.kernel_input_transform(wd, xd)
+    assert torch.equal(Ub, Ug) and torch.equal(Vb, Vg)
+    assert torch.equal(pb.input_transform(xd), Vg)
+    M = pb.contract(Vb, Ub, C)
+    assert torch.equal(pb.output_transform(M, N, H, W, K), pg.output_transform(M, N, H, W, K))
+    assert torch.equal(pb.conv2d(xd, wd), pg.conv2d(xd, wd))
