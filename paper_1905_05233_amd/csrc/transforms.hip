@@ -139,7 +139,18 @@ __global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, cons
 // rows and the workgroup's VALU work is spread over several waves.  Row
 // indices are compile-time constants in every wave (one template instance per
 // row group), which keeps the coefficients in scalar registers.
-constexpr int kInCh = 64;   // channels per workgroup, one per lane
+constexpr int kInCh = 64;   // LDS columns per workgroup, one per lane
+
+// channels per tile in a workgroup: 64, or fewer for narrow layers so that the
+// lanes still find work (Cp is a multiple of 8: 8, 16, 32 or 64)
+__host__ __device__ inline int input_column_width(int64_t Cp) {
+    return Cp >= 64 ? 64 : Cp > 16 ? 32 : Cp > 8 ? 16 : 8;
+}
+// workgroups (units) of the input transform
+inline int64_t input_units(const Geometry& g) {
+    const int cw = input_column_width(g.Cp);
+    return (g.T + kInCh / cw - 1) / (kInCh / cw) * ((g.Cp + cw - 1) / cw);
+}
 
 // rows per wave: the split that measured fastest for each alpha'
 constexpr int input_rows_per_wave(int alpha) { return alpha == 7 || alpha == 8 ? 2 : 3; }
@@ -206,31 +217,50 @@ __device__ __forceinline__ void input_transform_unit(const InputTable& tab, cons
     using P = InputShape<Elem, TT, ALPHA>;
     __shared__ __attribute__((aligned(16))) float win[TT * TT * kInCh];   // [u][v][64] fp32
 
-    const int64_t nch = (geo.Cp + kInCh - 1) / kInCh;
+    // the 64 LDS columns (one per lane) hold cw channels of 64 / cw tiles:
+    // cw = 64 for wide layers, the channel count rounded up to a power of two
+    // for narrow ones (C = 3: 8 tiles of 8 channels per workgroup)
+    const int cw = input_column_width(geo.Cp);
+    const int cwl = __builtin_ctz(cw);   // cw is a power of two
+    const int64_t nch = (geo.Cp + cw - 1) / cw;
     // XCD-aware numbering: the hardware deals workgroup ids round-robin to the
     // 8 XCDs; giving each XCD a contiguous run of units keeps neighbouring
     // tiles, whose windows overlap, in the same L2
     const int64_t unit = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
-    const int64_t tile = unit / nch;
-    const int64_t c0 = (unit % nch) * kInCh;
-    const int64_t tx = tile % geo.tw;
-    const int64_t ty = (tile / geo.tw) % geo.th;
-    const int64_t n = tile / (geo.tw * geo.th);
-    const int64_t h0 = ty * geo.m - 1;
-    const int64_t w0 = tx * geo.m - 1;
-    const Elem* xn = x + n * geo.H * geo.W * geo.C;
+    const int64_t tile0 = (unit / nch) * (kInCh / cw);
+    const int64_t c0 = (unit % nch) * cw;
+    const int tx0 = static_cast<int>(tile0 % geo.tw);
+    const int ty0 = static_cast<int>((tile0 / geo.tw) % geo.th);
+    const int n0 = static_cast<int>(tile0 / (geo.tw * geo.th));
+    const int tw = static_cast<int>(geo.tw), th = static_cast<int>(geo.th);
     const int tid = threadIdx.x;
 
     uint4 regs[P::kPer];
+    auto fetch = [&](bool wide) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < P::kPer; ++p) {
         const int ci = tid + p * P::kThreads;
         const int pix = ci / P::kChunksPerPix;
-        const int64_t hr = h0 + pix / TT;
-        const int64_t wc = w0 + pix % TT;
-        const int64_t cc = c0 + (ci % P::kChunksPerPix) * P::kChunkElems;
-        const bool in = ci < P::kChunks && hr >= 0 && hr < geo.H && wc >= 0 && wc < geo.W;
-        const Elem* src = xn + (hr * geo.W + wc) * geo.C + cc;
+        const int col = (ci % P::kChunksPerPix) * P::kChunkElems;   // first LDS column of the chunk
+        const int d = wide ? 0 : col >> cwl;   // tile of the workgroup, 0 .. 7
+        const int64_t tile = tile0 + d;
+        // coordinates of tile0 + d by carrying (no per-lane division); one
+        // carry at most unless a row has fewer than 8 tiles
+        int tx = tx0 + d, ty = ty0, n = n0;
+        if (!wide && tx >= tw) {
+            do {
+                tx -= tw;
+                if (++ty == th) {
+                    ty = 0;
+                    ++n;
+                }
+            } while (tx >= tw);
+        }
+        const int64_t hr = static_cast<int64_t>(ty) * geo.m - 1 + pix / TT;
+        const int64_t wc = static_cast<int64_t>(tx) * geo.m - 1 + pix % TT;
+        const int64_t cc = c0 + (wide ? col : col & (cw - 1));
+        const bool in = ci < P::kChunks && tile < geo.T && hr >= 0 && hr < geo.H && wc >= 0 && wc < geo.W;
+        const Elem* src = x + ((static_cast<int64_t>(n) * geo.H + hr) * geo.W + wc) * geo.C + cc;
         if constexpr (kWhole) {
             regs[p] = (in && cc < geo.C) ? *reinterpret_cast<const uint4*>(src) : uint4{0u, 0u, 0u, 0u};
         } else {
@@ -240,6 +270,10 @@ __device__ __forceinline__ void input_transform_unit(const InputTable& tab, cons
             regs[p] = __builtin_bit_cast(uint4, e);
         }
     }
+    };
+    // wide layers (one tile per workgroup) keep the tile coordinates uniform
+    if (cw == kInCh) fetch(true);
+    else fetch(false);
 #pragma unroll
     for (int p = 0; p < P::kPer; ++p) {
         const int ci = tid + p * P::kThreads;
@@ -253,8 +287,9 @@ __device__ __forceinline__ void input_transform_unit(const InputTable& tab, cons
 
     const int c = tid % kInCh;
     const int g = __builtin_amdgcn_readfirstlane(tid / kInCh);
-    const int64_t cg = c0 + c;
-    if (cg >= geo.Cp) return;
+    const int64_t tile = tile0 + (c >> cwl);
+    const int64_t cg = c0 + (c & (cw - 1));
+    if (tile >= geo.T || cg >= geo.Cp) return;
     // channels C..Cp-1 read as zero and so store zeros
     input_row_groups<Elem, TT, ALPHA, P::kR, CO>(g, tab, win + c, V + tile * geo.Cp + cg, geo.T * geo.Cp,
                                                  std::make_integer_sequence<int, P::kG>{});
@@ -410,7 +445,7 @@ hipError_t launch_kernel_transform_t(const Geometry& g, const KernelTable& tab, 
 template <typename Elem, int TT, int A, class CO>
 hipError_t launch_it(const Geometry& g, const InputTable& tab, const Elem* xp, Elem* vp, hipStream_t stream) {
     constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
-    const int64_t units = g.T * ((g.Cp + kInCh - 1) / kInCh);
+    const int64_t units = input_units(g);
     if (units > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(units)), block(InputShape<Elem, TT, A>::kThreads);
     if (g.C % kChunkElems == 0)
@@ -425,7 +460,7 @@ hipError_t launch_kit(const Geometry& g, const KernelTable& ktab, const InputTab
                       const Elem* xp, Elem* up, Elem* vp, hipStream_t stream) {
     constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
     constexpr int kThr = InputShape<Elem, TT, A>::kThreads;
-    const int64_t units = g.T * ((g.Cp + kInCh - 1) / kInCh);
+    const int64_t units = input_units(g);
     const int64_t kt_runs = static_cast<int64_t>(g.alpha) * g.K * (g.Cp / 4);
     // a multiple of 8, so the input transform's ids keep their XCD (id mod 8)
     const int64_t n_kt = (kt_runs + 8 * kThr - 1) / (8 * kThr) * 8;
