@@ -114,19 +114,30 @@ __device__ __forceinline__ u32x4 lds_read16(const unsigned char* p) {
     return v;
 }
 
-// wait for this wave's LDS reads; the operands tie the values to the wait
+// wait for this wave's LDS reads; the operands tie the values to the wait.
+// Every operand must be a different variable: one bound twice gets a copy
+// made before the wait, which reads the register while its load is in flight.
 __device__ __forceinline__ void lds_settle(u32x4& a, u32x4& b, u32x4& c, u32x4& d) {
     asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : : "memory");
+}
+__device__ __forceinline__ void lds_settle(u32x4& a, u32x4& b, u32x4& c, u32x4& d, u32x4& e, u32x4& f) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d), "+v"(e), "+v"(f) : : "memory");
+}
+__device__ __forceinline__ void lds_settle(u32x4& a, u32x4& b, u32x4& c) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c) : : "memory");
+}
+__device__ __forceinline__ void lds_settle(u32x4& a, u32x4& b) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b) : : "memory");
 }
 
 // s_waitcnt immediate that waits until at most n vector-memory operations of
 // this wave are outstanding (gfx9 encoding; expcnt and lgkmcnt not waited on)
 constexpr int vm_wait(int n) { return (n & 0xf) | (0x7 << 4) | (0xf << 8) | (((n >> 4) & 0x3) << 14); }
 
-template <int D, int MM, int ALPHA, int WT>
+template <int D, int MM, int ALPHA, int WT, bool NARROW>
 __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
     const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, typename DTypeOf<D>::type* __restrict__ y,
-    OutputTable tab, Geometry geo, int kw, int n_kb, int rb, int n_slices) {
+    OutputTable tab, Geometry geo, int kw, int n_kb, int rb, int n_slices, int xp) {
     using Elem = typename DTypeOf<D>::type;
     using S = Storage<Elem>;
     // four LDS stages (one step each, three steps in flight), separate arrays
@@ -166,10 +177,19 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
     // (channel rows first, then tile rows; whole instructions, since both
     // counts are multiples of 16, so the choice of operand is uniform).  Lane l
     // lands at row 8 (w + 4 j) + l / 8, 16-byte column l % 8, and fetches the
-    // row's piece (l % 8) ^ (l / 8): an XOR swizzle that keeps the fragment
-    // reads conflict-free without padding.  Instructions past the block's rows
-    // write zeros (every wave issues the same count, so one vmcnt fits all).
-    const int piece = ((lane & 7) ^ (lane >> 3)) * 16;
+    // row's piece lp = (l % 8) ^ (l / 8): an XOR swizzle that keeps the
+    // fragment reads conflict-free without padding.  Instructions past the
+    // block's rows write zeros (every wave issues the same count, so one
+    // vmcnt fits all).
+    //
+    // Narrow rows (xp > 1, a row of at most 64 bytes): a step holds xp domain
+    // points, each in ppr = 8 / xp consecutive pieces of the slice, so the
+    // DMAs and barriers per domain point drop xp-fold.  Piece lp then belongs
+    // to the step's domain point lp / ppr, byte 16 (lp % ppr) of its row.
+    const int ppr = 8 / xp;
+    const int lp = (lane & 7) ^ (lane >> 3);
+    const int lxi = lp / ppr;                   // domain point of the piece within the step (0 if wide)
+    const int piece = (lp % ppr) * 16;          // byte offset of the piece within its row
     uint32_t roff[kDmaPerWave];
     bool live[kDmaPerWave], isu[kDmaPerWave];
 #pragma unroll
@@ -180,14 +200,32 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
         const int row = r8 + (lane >> 3);
         roff[j] = static_cast<uint32_t>((row < krows ? row : row - krows) * rb + piece);
     }
-    auto issue = [&](unsigned char* st, int xi, int sl, bool any) {
-        const auto ru = make_rsrc(U + (static_cast<int64_t>(xi) * K + k0) * rb, (K - k0) * rb);
-        const auto rv = make_rsrc(V + (static_cast<int64_t>(xi) * T + t0) * rb, (T - t0) * rb);
-        const int sb = sl * kSlice;
-        const bool in = any && sb + piece < rb;   // zero past the row
+    // wide: the request is (xi, slice); narrow: the step's first domain point
+    // in visiting order (a fastest), each lane's plane found from its lxi
+    auto issue = [&](unsigned char* st, int xi, int sl, int q0, bool any) __attribute__((always_inline)) {
+        if constexpr (!NARROW) {
+            const auto ru = make_rsrc(U + (static_cast<int64_t>(xi) * K + k0) * rb, (K - k0) * rb);
+            const auto rv = make_rsrc(V + (static_cast<int64_t>(xi) * T + t0) * rb, (T - t0) * rb);
+            const int sb = sl * kSlice;
+            const bool in = any && sb + piece < rb;   // zero past the row
 #pragma unroll
-        for (int j = 0; j < kDmaPerWave; ++j)
-            dma16(isu[j] ? ru : rv, st + (wave + 4 * j) * 1024, live[j] && in ? roff[j] + sb : kOob);
+            for (int j = 0; j < kDmaPerWave; ++j)
+                dma16(isu[j] ? ru : rv, st + (wave + 4 * j) * 1024, live[j] && in ? roff[j] + sb : kOob);
+        } else {
+            // descriptors over every plane (checked to fit 32-bit offsets at
+            // launch); rows past T or K read other planes' rows, which only
+            // reach (channel, tile) pairs that are never stored
+            const auto ru = make_rsrc(U + k0 * rb, (static_cast<int64_t>(ALPHA) * ALPHA * K - k0) * rb);
+            const auto rv = make_rsrc(V + t0 * rb, (static_cast<int64_t>(ALPHA) * ALPHA * T - t0) * rb);
+            const int q = q0 + lxi;                         // this lane's domain point, in visiting order
+            const int pxi = (q % ALPHA) * ALPHA + q / ALPHA;  // its index xi = a alpha' + b
+            const bool in = any && q < ALPHA * ALPHA && piece < rb;
+            const uint32_t pu = static_cast<uint32_t>(pxi * K * rb), pv = static_cast<uint32_t>(pxi * T * rb);
+#pragma unroll
+            for (int j = 0; j < kDmaPerWave; ++j)
+                dma16(isu[j] ? ru : rv, st + (wave + 4 * j) * 1024,
+                      live[j] && in ? roff[j] + (isu[j] ? pu : pv) : kOob);
+        }
     };
 
     f32x4 acc[WT];
@@ -212,10 +250,11 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
     const int b_row = (krows + wt * 16 * WT + l16) * kSlice;
     const int col0 = ((grp) ^ swz) * 16;       // slice half 0: pieces 0..3
     const int col1 = ((grp + 4) ^ swz) * 16;   // slice half 1: pieces 4..7
-    const int nsteps = ALPHA * ALPHA * n_slices;
+    const int nsteps = NARROW ? (ALPHA * ALPHA + xp - 1) / xp : ALPHA * ALPHA * n_slices;
     // step order: slices fastest, then a (M row), then b (M column)
-    int a = 0, bc = 0, sl = 0;      // step being computed
-    int na = 0, nb = 0, ns = 0;     // next step to request
+    int a = 0, bc = 0, sl = 0;      // step being computed (the next domain point to fold when narrow)
+    int na = 0, nb = 0, ns = 0;     // next step to request (wide)
+    int nq = 0;                     // first domain point of the next step to request (narrow)
     auto advance = [&](int& a_, int& b_, int& s_) {
         if (++s_ == n_slices) {
             s_ = 0;
@@ -225,12 +264,17 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
             }
         }
     };
-    auto request = [&](unsigned char* st) {
+    auto request = [&](unsigned char* st) __attribute__((always_inline)) {
         // past the last step the group is issued anyway (all zeros), which
         // keeps the outstanding count per step constant
-        const bool any = nb < ALPHA;
-        issue(st, any ? na * ALPHA + nb : 0, any ? ns : 0, any);
-        if (any) advance(na, nb, ns);
+        if constexpr (!NARROW) {
+            const bool any = nb < ALPHA;
+            issue(st, any ? na * ALPHA + nb : 0, any ? ns : 0, 0, any);
+            if (any) advance(na, nb, ns);
+        } else {
+            issue(st, 0, 0, nq, nq < ALPHA * ALPHA);
+            nq += xp;
+        }
     };
 
     // two-level channel sum: each step's slice goes into a fresh accumulator
@@ -291,6 +335,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
     };
 
     bool have_prev = false;
+    int sq = 0;   // first domain point of the step being computed (narrow)
     auto step = [&](const unsigned char* cur, unsigned char* nxt) __attribute__((always_inline)) {
         // this wave's DMAs for `cur` are done once at most two groups remain;
         // the barrier makes every wave's visible and frees `nxt` (read in the
@@ -302,23 +347,55 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
         // the coefficients must be in registers before the LDS reads go out
 #pragma unroll
         for (int o = 0; o < MM; ++o) asm volatile("" : "+s"(cz[o]), "+s"(cy[o]));
-        u32x4 fa0 = lds_read16(cur + a_row + col0);
-        u32x4 fa1 = lds_read16(cur + a_row + col1);
-        u32x4 fb[WT][2];
+        if constexpr (!NARROW) {
+            u32x4 fa0 = lds_read16(cur + a_row + col0);
+            u32x4 fa1 = lds_read16(cur + a_row + col1);
+            u32x4 fb[WT][2];
 #pragma unroll
-        for (int w = 0; w < WT; ++w) {
-            fb[w][0] = lds_read16(cur + b_row + w * 16 * kSlice + col0);
-            fb[w][1] = lds_read16(cur + b_row + w * 16 * kSlice + col1);
+            for (int w = 0; w < WT; ++w) {
+                fb[w][0] = lds_read16(cur + b_row + w * 16 * kSlice + col0);
+                fb[w][1] = lds_read16(cur + b_row + w * 16 * kSlice + col1);
+            }
+            if (have_prev) fold();
+            have_prev = true;
+            if constexpr (WT == 2) lds_settle(fa0, fa1, fb[0][0], fb[0][1], fb[1][0], fb[1][1]);
+            else lds_settle(fa0, fa1, fb[0][0], fb[0][1]);
+#pragma unroll
+            for (int w = 0; w < WT; ++w) {
+                part[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                mma<D>(fa0, fb[w][0], part[w]);
+                mma<D>(fa1, fb[w][1], part[w]);
+            }
+        } else {
+        // narrow: domain point i of the step sits in pieces [i ppr, i ppr + ppr)
+        // of one slice half; lane groups outside them contribute zeros
+        for (int i = 0; i < xp; ++i) {
+            if (sq + i >= ALPHA * ALPHA) break;
+            if (i > 0) {
+                // the coefficients loaded at the end of the last iteration,
+                // in registers before this iteration's LDS reads go out
+#pragma unroll
+                for (int o = 0; o < MM; ++o) asm volatile("" : "+s"(cz[o]), "+s"(cy[o]));
+            }
+            const int p0 = i * ppr;
+            const int col = (((p0 & 4) + grp) ^ swz) * 16;
+            u32x4 fa = lds_read16(cur + a_row + col);
+            u32x4 fb[WT];
+#pragma unroll
+            for (int w = 0; w < WT; ++w) fb[w] = lds_read16(cur + b_row + w * 16 * kSlice + col);
+            if (have_prev) fold();
+            have_prev = true;
+            coefs();   // for the fold of this domain point, in the next iteration
+            if constexpr (WT == 2) lds_settle(fa, fb[0], fb[1]);
+            else lds_settle(fa, fb[0]);
+            if (static_cast<unsigned>(grp - (p0 & 3)) >= static_cast<unsigned>(ppr)) fa = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int w = 0; w < WT; ++w) {
+                part[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                mma<D>(fa, fb[w], part[w]);
+            }
         }
-        if (have_prev) fold();
-        have_prev = true;
-        if constexpr (WT == 2) lds_settle(fa0, fa1, fb[0][0], fb[1][1]), lds_settle(fb[0][1], fb[1][0], fa0, fa1);
-        else lds_settle(fa0, fa1, fb[0][0], fb[0][1]);
-#pragma unroll
-        for (int w = 0; w < WT; ++w) {
-            part[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            mma<D>(fa0, fb[w][0], part[w]);
-            mma<D>(fa1, fb[w][1], part[w]);
+        sq += xp;
         }
     };
 
@@ -407,15 +484,22 @@ hipError_t launch_contract_output_t<WG_DTYPE>(const Geometry& g, const OutputTab
     const int64_t n_tb = (g.T + 16 * wt * (4 / kw) - 1) / (16 * wt * (4 / kw));
     const int64_t grid = n_kb * n_tb;
     if (grid > 0x7fffffff) return hipErrorInvalidValue;
-    const int n_slices = (rb + kSlice - 1) / kSlice;
+    // rows of at most 64 bytes: several domain points per step (all planes
+    // addressed with 32-bit offsets); else one 128-byte slice per step
+    int xp = 1;
+    const int64_t a2 = static_cast<int64_t>(g.alpha) * g.alpha;
+    if (rb <= 64 && a2 * g.T * rb < 0xffff0000LL && a2 * g.K * rb < 0xffff0000LL) xp = rb <= 16 ? 8 : rb <= 32 ? 4 : 2;
+    const int n_slices = xp > 1 ? 1 : (rb + kSlice - 1) / kSlice;
     const auto* vp = static_cast<const unsigned char*>(V);
     const auto* up = static_cast<const unsigned char*>(U);
     auto* yp = static_cast<Elem*>(y);
     const unsigned nb = static_cast<unsigned>(grid);
+#define WG_CO_LAUNCH(TT, A, W, NAR)                                                                       \
+    hipLaunchKernelGGL((contract_output_kernel<D, TT - 2, A, W, NAR>), dim3(nb), dim3(kThreads), 0, stream, vp, \
+                       up, yp, tab, g, kw, n_kb, rb, n_slices, xp);
 #define WG_CO_CASE(TT, A, W)                                                                              \
     if (g.t == TT && g.alpha == A && wt == W) {                                                           \
-        hipLaunchKernelGGL((contract_output_kernel<D, TT - 2, A, W>), dim3(nb), dim3(kThreads), 0, stream, vp, \
-                           up, yp, tab, g, kw, n_kb, rb, n_slices);                                       \
+        if (xp > 1) WG_CO_LAUNCH(TT, A, W, true) else WG_CO_LAUNCH(TT, A, W, false)                       \
         return hipGetLastError();                                                                         \
     }
     WG_CO_CASE(4, 4, 1) WG_CO_CASE(4, 5, 1) WG_CO_CASE(4, 6, 1) WG_CO_CASE(4, 7, 1)
@@ -424,6 +508,7 @@ hipError_t launch_contract_output_t<WG_DTYPE>(const Geometry& g, const OutputTab
     WG_CO_CASE(6, 6, 2) WG_CO_CASE(6, 7, 2) WG_CO_CASE(6, 8, 2) WG_CO_CASE(6, 9, 2)
     WG_CO_CASE(8, 8, 1) WG_CO_CASE(8, 9, 1) WG_CO_CASE(8, 10, 1) WG_CO_CASE(8, 11, 1) WG_CO_CASE(8, 12, 1)
 #undef WG_CO_CASE
+#undef WG_CO_LAUNCH
     return hipErrorInvalidValue;
 }
 
