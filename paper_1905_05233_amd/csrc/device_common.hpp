@@ -59,4 +59,42 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
                                              static_cast<int>(kRsrcWord3));
 }
 
+// --- LDS fragment reads issued from inline assembly ------------------------
+// The compiler inserts its waits for LDS reads it issues itself, and cannot
+// tell the buffers of a software pipeline apart; reads issued from inline
+// assembly are waited for explicitly with lds_settle*, whose in/out operands
+// tie the values to the wait.  LDS reads of a wave complete in issue order,
+// so lgkmcnt(n) means every read except the last n issued has arrived (scalar
+// loads in flight only lower that count).  Every operand of one wait must be
+// a different variable: one bound twice gets a copy made before the wait,
+// which reads the register while its load is still in flight.
+typedef unsigned int lds_u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ lds_u32x4 lds_read16(const unsigned char* p) {
+    const uint32_t a = static_cast<uint32_t>(
+        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const unsigned char*)p));
+    lds_u32x4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+    return v;
+}
+
+// wait for every LDS read of this wave
+__device__ __forceinline__ void lds_settle(lds_u32x4& a, lds_u32x4& b) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b) : : "memory");
+}
+__device__ __forceinline__ void lds_settle(lds_u32x4& a, lds_u32x4& b, lds_u32x4& c) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c) : : "memory");
+}
+__device__ __forceinline__ void lds_settle(lds_u32x4& a, lds_u32x4& b, lds_u32x4& c, lds_u32x4& d) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : : "memory");
+}
+__device__ __forceinline__ void lds_settle(lds_u32x4& a, lds_u32x4& b, lds_u32x4& c, lds_u32x4& d, lds_u32x4& e,
+                                           lds_u32x4& f) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d), "+v"(e), "+v"(f) : : "memory");
+}
+// wait for all but the last two LDS reads of this wave
+__device__ __forceinline__ void lds_settle_but2(lds_u32x4& a, lds_u32x4& b) {
+    asm volatile("s_waitcnt lgkmcnt(2)" : "+v"(a), "+v"(b) : : "memory");
+}
+
 }  // namespace wg

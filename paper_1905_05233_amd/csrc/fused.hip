@@ -103,33 +103,6 @@ __device__ __forceinline__ void lds_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// 16-byte LDS read issued from inline assembly, so the compiler does not
-// insert its own wait for the DMAs in flight (it cannot tell the stages
-// apart across iterations); the caller waits with lds_settle before use.
-__device__ __forceinline__ u32x4 lds_read16(const unsigned char* p) {
-    const uint32_t a = static_cast<uint32_t>(
-        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const unsigned char*)p));
-    u32x4 v;
-    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
-    return v;
-}
-
-// wait for this wave's LDS reads; the operands tie the values to the wait.
-// Every operand must be a different variable: one bound twice gets a copy
-// made before the wait, which reads the register while its load is in flight.
-__device__ __forceinline__ void lds_settle(u32x4& a, u32x4& b, u32x4& c, u32x4& d) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : : "memory");
-}
-__device__ __forceinline__ void lds_settle(u32x4& a, u32x4& b, u32x4& c, u32x4& d, u32x4& e, u32x4& f) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d), "+v"(e), "+v"(f) : : "memory");
-}
-__device__ __forceinline__ void lds_settle(u32x4& a, u32x4& b, u32x4& c) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c) : : "memory");
-}
-__device__ __forceinline__ void lds_settle(u32x4& a, u32x4& b) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b) : : "memory");
-}
-
 // s_waitcnt immediate that waits until at most n vector-memory operations of
 // this wave are outstanding (gfx9 encoding; expcnt and lgkmcnt not waited on)
 constexpr int vm_wait(int n) { return (n & 0xf) | (0x7 << 4) | (0xf << 8) | (((n >> 4) & 0x3) << 14); }

@@ -1,16 +1,19 @@
-"""The fused contraction issues its LDS fragment reads from inline assembly and
-waits for them with a separate inline-assembly wait, so the compiler's own
-wait insertion cannot see them.  Correctness then rests on one property of
-the generated code: no vector instruction reads or writes a register that an
-in-flight ``ds_read_b128`` is still filling.  A register copy placed before
-the wait (which the compiler makes, for instance, when one variable is bound
-to two operands of the wait) breaks it, and shows up on the GPU only as rare
-wrong values.
+"""The fused contraction issues its LDS fragment reads, and the global loads of
+its U fragments, from inline assembly and waits for them with separate
+inline-assembly waits, so the compiler's own wait insertion cannot see them.
+Correctness then rests on one property of the generated code: no vector
+instruction reads or writes a register that an in-flight ``ds_read_b128`` or
+buffer load is still filling.  A register copy placed before the wait (which
+the compiler makes, for instance, when one variable is bound to two operands
+of the wait) breaks it, and shows up on the GPU only as rare wrong values.
 
 This test compiles the kernel to gfx950 assembly on the CPU, one build per
 storage dtype, and checks the property with a forward dataflow pass over the
-basic blocks of each kernel (a register is pending from its read until the
-next ``s_waitcnt lgkmcnt(0)`` on every path).
+basic blocks of each kernel.  LDS reads of a wave complete in issue order, so
+after ``s_waitcnt lgkmcnt(n)`` only the last n reads issued may still be
+pending (scalar loads counted by the same counter only make fewer pending);
+likewise vector-memory operations (loads, stores and buffer-to-LDS loads)
+under ``vmcnt``.
 """
 import os
 import re
@@ -21,13 +24,11 @@ import pytest
 
 from paper_1905_05233_amd import build_native as B
 
-FUSED = os.path.join(B.CSRC, "fused.hip")
 
-
-def _device_asm(dtype_code, out_dir):
-    out = os.path.join(out_dir, f"fused_{dtype_code}.s")
-    cmd = ([B.HIPCC] + B.COMMON + B.DEVICE + [f"-DWG_DTYPE={dtype_code}", "--cuda-device-only", "-S", FUSED,
-                                                "-o", out])
+def _device_asm(source, dtype_code, out_dir):
+    out = os.path.join(out_dir, f"{source}_{dtype_code}.s")
+    cmd = ([B.HIPCC] + B.COMMON + B.DEVICE + [f"-DWG_DTYPE={dtype_code}", "--cuda-device-only", "-S",
+                                                os.path.join(B.CSRC, f"{source}.hip"), "-o", out])
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     with open(out) as f:
@@ -66,8 +67,20 @@ def _blocks(code):
     return blocks
 
 
+def _vmem_dest(ins):
+    """Destination registers of a vector-memory load into VGPRs (none for stores
+    and for the buffer-to-LDS form, whose first operand is an address)."""
+    m = re.match(r"^(buffer|global|flat)_load_\w+\s+(v\[(\d+):(\d+)\]|v(\d+))", ins)
+    if not m or ins.rstrip().endswith(" lds"):
+        return frozenset()
+    if m.group(3) is not None:
+        return frozenset(range(int(m.group(3)), int(m.group(4)) + 1))
+    return frozenset([int(m.group(5))])
+
+
 def lds_read_hazards(asm):
-    """(kernel, instruction) pairs that touch a register of an LDS read in flight."""
+    """(kernel, instruction) pairs that touch a register of an LDS read or a
+    vector-memory load in flight."""
     body = asm[:asm.index("amdhsa.kernels")] if "amdhsa.kernels" in asm else asm
     parts = re.split(r"\n(_Z\S+):[^\n]*\n", body)
     found, kernels = [], 0
@@ -86,26 +99,45 @@ def lds_read_hazards(asm):
             if not last.startswith(("s_branch", "s_endpgm", "s_setpc")) and k + 1 < len(blocks):
                 nxt.append(k + 1)
             succ.append(nxt)
-        entry = [set() for _ in blocks]
+        # state: for each depth d (0 = youngest), the registers of reads that may
+        # be pending with d younger reads issued after them; merged by union
+        # two in-order queues (LDS reads under lgkmcnt, vector memory under vmcnt)
+        depth = 64
+        empty = tuple(frozenset() for _ in range(depth))
+        entry = [(empty, empty) for _ in blocks]
         work, hits = list(range(len(blocks))), set()
         while work:
             k = work.pop(0)
-            pending = set(entry[k])
+            lgkm, vm = list(entry[k][0]), list(entry[k][1])
             for ins in blocks[k][1]:
+                live = frozenset().union(*lgkm, *vm)
+                if live and not ins.startswith("s_"):
+                    operands = ins.split(None, 1)[1] if " " in ins else ""
+                    regs = _vregs(operands)
+                    if ins.startswith(("buffer_", "global_", "flat_")):
+                        regs = regs - _vmem_dest(ins)   # a load's own destination is not a use
+                    if regs & live:
+                        hits.add((name, ins))
                 m = re.match(r"^ds_read_b128\s+v\[(\d+):(\d+)\]", ins)
                 if m:
-                    pending |= set(range(int(m.group(1)), int(m.group(2)) + 1))
+                    lgkm = [frozenset(range(int(m.group(1)), int(m.group(2)) + 1))] + lgkm[:depth - 1]
                     continue
-                if ins.startswith("s_waitcnt") and "lgkmcnt(0)" in ins:
-                    pending = set()
+                if ins.startswith(("buffer_", "global_", "flat_")):
+                    vm = [_vmem_dest(ins)] + vm[:depth - 1]
                     continue
-                if pending and not ins.startswith("s_"):
-                    operands = ins.split(None, 1)[1] if " " in ins else ""
-                    if _vregs(operands) & pending:
-                        hits.add((name, ins))
+                if ins.startswith("s_waitcnt"):
+                    w = re.search(r"lgkmcnt\((\d+)\)", ins)
+                    if w:
+                        n = int(w.group(1))
+                        lgkm = lgkm[:n] + [frozenset()] * (depth - n)
+                    w = re.search(r"vmcnt\((\d+)\)", ins)
+                    if w:
+                        n = int(w.group(1))
+                        vm = vm[:n] + [frozenset()] * (depth - n)
             for j in succ[k]:
-                if not pending <= entry[j]:
-                    entry[j] |= pending
+                new = (tuple(a | b for a, b in zip(entry[j][0], lgkm)), tuple(a | b for a, b in zip(entry[j][1], vm)))
+                if new != entry[j]:
+                    entry[j] = new
                     if j not in work:
                         work.append(j)
         found.extend(sorted(hits))
@@ -114,7 +146,8 @@ def lds_read_hazards(asm):
 
 def test_scanner_flags_a_copy_before_the_wait():
     """The scanner itself: a copy of an in-flight fragment across a branch is found,
-    the same code with the wait first is not."""
+    the same code with the wait first is not; a counted wait covers all but the
+    youngest reads."""
     bad = """
 _Zk:                                    ; @_Zk
 \tds_read_b128 v[12:15], v48
@@ -130,13 +163,37 @@ _Zk:                                    ; @_Zk
                        "\ts_waitcnt lgkmcnt(0)\n\tv_mov_b64_e32 v[8:9], v[12:13]\n")
     assert lds_read_hazards(bad) == (1, [("_Zk", "v_mov_b64_e32 v[8:9], v[12:13]")])
     assert lds_read_hazards(good) == (1, [])
+    counted = """
+_Zk:                                    ; @_Zk
+\tds_read_b128 v[12:15], v48
+\tds_read_b128 v[16:19], v49
+\tds_read_b128 v[20:23], v50
+\ts_waitcnt lgkmcnt(1)
+\tv_mfma_f32_16x16x32_bf16 v[0:3], v[12:15], v[16:19], 0
+\tv_mov_b32_e32 v24, v21
+\ts_endpgm
+"""
+    assert lds_read_hazards(counted) == (1, [("_Zk", "v_mov_b32_e32 v24, v21")])
+    vmem = """
+_Zk:                                    ; @_Zk
+\tbuffer_load_dwordx4 v[12:15], v40, s[0:3], 0 offen
+\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds
+\tbuffer_load_dwordx4 v[16:19], v41, s[0:3], 0 offen
+\ts_waitcnt vmcnt(2)
+\tv_mov_b32_e32 v20, v13
+\tv_mov_b32_e32 v21, v17
+\ts_endpgm
+"""
+    assert lds_read_hazards(vmem) == (1, [("_Zk", "v_mov_b32_e32 v21, v17")])
 
 
 @pytest.mark.skipif(not os.path.exists(B.HIPCC), reason="hipcc not installed")
-def test_fused_kernel_waits_before_using_lds_fragments(tmp_path):
+@pytest.mark.parametrize("source,dtypes,min_kernels", [("fused", (0, 1, 2), 40)])
+def test_kernels_wait_before_using_lds_fragments(source, dtypes, min_kernels, tmp_path):
+    """One build per storage dtype (the source is compiled with WG_DTYPE set)."""
     with ThreadPoolExecutor(3) as ex:
-        asms = list(ex.map(lambda d: _device_asm(d, str(tmp_path)), [0, 1, 2]))
-    for code, asm in enumerate(asms):
+        asms = list(ex.map(lambda d: _device_asm(source, d, str(tmp_path)), dtypes))
+    for code, asm in zip(dtypes, asms):
         kernels, hits = lds_read_hazards(asm)
-        assert kernels >= 40, f"dtype {code}: only {kernels} kernels found in the assembly"
-        assert not hits, f"dtype {code}: {len(hits)} uses of in-flight LDS fragments, e.g. {hits[:3]}"
+        assert kernels >= min_kernels, f"{source} dtype {code}: only {kernels} kernels found in the assembly"
+        assert not hits, f"{source} dtype {code}: {len(hits)} uses of in-flight LDS fragments, e.g. {hits[:3]}"
