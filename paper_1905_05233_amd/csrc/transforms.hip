@@ -146,10 +146,29 @@ constexpr int kInCh = 64;   // LDS columns per workgroup, one per lane
 __host__ __device__ inline int input_column_width(int64_t Cp) {
     return Cp >= 64 ? 64 : Cp > 16 ? 32 : Cp > 8 ? 16 : 8;
 }
-// workgroups (units) of the input transform
-inline int64_t input_units(const Geometry& g) {
+// Tiles a wide-layer workgroup walks in turn (PT, a template parameter of
+// the kernel: the next window is fetched while the current one is
+// transformed).  PT = kInTiles for layers with many units (fewer,
+// longer-lived workgroups); PT = 1 for small ones, which spreads them over
+// more CUs and keeps the leaner single-tile instance (fewer registers).
+constexpr int kInTiles = 4;
+constexpr int64_t kInManyUnits = 8192;
+// tiles per unit: PT in turn for wide layers, 64 / cw side by side for narrow ones
+__host__ __device__ inline int input_tiles_per_unit(int64_t Cp, int pt) {
+    const int cw = input_column_width(Cp);
+    return cw == kInCh ? pt : kInCh / cw;
+}
+// the PT instance a layer runs (whole: C is a multiple of the 16-byte chunk)
+inline int input_pt(const Geometry& g, bool whole) {
     const int cw = input_column_width(g.Cp);
-    return (g.T + kInCh / cw - 1) / (kInCh / cw) * ((g.Cp + cw - 1) / cw);
+    if (!whole || cw != kInCh) return 1;
+    return g.T * ((g.Cp + cw - 1) / cw) >= kInManyUnits ? kInTiles : 1;
+}
+// workgroups (units) of the input transform
+inline int64_t input_units(const Geometry& g, int pt) {
+    const int cw = input_column_width(g.Cp);
+    const int nt = input_tiles_per_unit(g.Cp, pt);
+    return (g.T + nt - 1) / nt * ((g.Cp + cw - 1) / cw);
 }
 
 // rows per wave: the split that measured fastest for each alpha'
@@ -209,7 +228,7 @@ __device__ __forceinline__ void input_row_groups(int g, const InputTable& tab, c
 
 // kWhole: C is a multiple of the 16-byte chunk width, so a chunk lies wholly
 // inside or wholly past C; otherwise the window is fetched element by element.
-template <typename Elem, int TT, int ALPHA, bool kWhole, class CO>
+template <typename Elem, int TT, int ALPHA, bool kWhole, class CO, int PT>
 __device__ __forceinline__ void input_transform_unit(const InputTable& tab, const Elem* __restrict__ x,
                                                      Elem* __restrict__ V, const Geometry& geo, int64_t bid,
                                                      int64_t G) {
@@ -227,24 +246,29 @@ __device__ __forceinline__ void input_transform_unit(const InputTable& tab, cons
     // 8 XCDs; giving each XCD a contiguous run of units keeps neighbouring
     // tiles, whose windows overlap, in the same L2
     const int64_t unit = (G % 8 == 0) ? (bid % 8) * (G / 8) + bid / 8 : bid;
-    const int64_t tile0 = (unit / nch) * (kInCh / cw);
+    const int per = input_tiles_per_unit(geo.Cp, PT);
+    const int64_t tile0 = (unit / nch) * per;
     const int64_t c0 = (unit % nch) * cw;
-    const int tx0 = static_cast<int>(tile0 % geo.tw);
-    const int ty0 = static_cast<int>((tile0 / geo.tw) % geo.th);
-    const int n0 = static_cast<int>(tile0 / (geo.tw * geo.th));
     const int tw = static_cast<int>(geo.tw), th = static_cast<int>(geo.th);
     const int tid = threadIdx.x;
+    // coordinates of the unit's first tile (the walking loop carries them on)
+    int tx0 = static_cast<int>(tile0 % geo.tw);
+    int ty0 = static_cast<int>((tile0 / geo.tw) % geo.th);
+    int n0 = static_cast<int>(tile0 / (geo.tw * geo.th));
 
     uint4 regs[P::kPer];
-    auto fetch = [&](bool wide) __attribute__((always_inline)) {
+    // the window of tile t at (tx0, ty0, n0) (wide: 64 channels of one tile;
+    // narrow: cw channels of tiles t .. t + 64 / cw - 1, one per group of cw
+    // LDS columns)
+    auto fetch = [&](int64_t t, bool wide) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < P::kPer; ++p) {
         const int ci = tid + p * P::kThreads;
         const int pix = ci / P::kChunksPerPix;
         const int col = (ci % P::kChunksPerPix) * P::kChunkElems;   // first LDS column of the chunk
         const int d = wide ? 0 : col >> cwl;   // tile of the workgroup, 0 .. 7
-        const int64_t tile = tile0 + d;
-        // coordinates of tile0 + d by carrying (no per-lane division); one
+        const int64_t tile = t + d;
+        // coordinates of t + d by carrying (no per-lane division); one
         // carry at most unless a row has fewer than 8 tiles
         int tx = tx0 + d, ty = ty0, n = n0;
         if (!wide && tx >= tw) {
@@ -271,41 +295,74 @@ __device__ __forceinline__ void input_transform_unit(const InputTable& tab, cons
         }
     }
     };
-    // wide layers (one tile per workgroup) keep the tile coordinates uniform
-    if (cw == kInCh) fetch(true);
-    else fetch(false);
+    auto park = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int p = 0; p < P::kPer; ++p) {
-        const int ci = tid + p * P::kThreads;
-        if (ci < P::kChunks) {
-            const Elem* e = reinterpret_cast<const Elem*>(&regs[p]);
+        for (int p = 0; p < P::kPer; ++p) {
+            const int ci = tid + p * P::kThreads;
+            if (ci < P::kChunks) {
+                const Elem* e = reinterpret_cast<const Elem*>(&regs[p]);
 #pragma unroll
-            for (int k = 0; k < P::kChunkElems; ++k) win[ci * P::kChunkElems + k] = S::to_f32(e[k]);
+                for (int k = 0; k < P::kChunkElems; ++k) win[ci * P::kChunkElems + k] = S::to_f32(e[k]);
+            }
         }
-    }
-    __syncthreads();
+    };
 
     const int c = tid % kInCh;
     const int g = __builtin_amdgcn_readfirstlane(tid / kInCh);
+    // channels C..Cp-1 read as zero and so store zeros
+    if (PT > 1 && cw == kInCh) {
+        // wide, PT > 1: PT consecutive tiles in turn; the next window is in
+        // flight while the current one is transformed (the loop is unrolled,
+        // so the compiler's waits for the window loads are exact)
+        const int64_t cg = c0 + c;
+        fetch(tile0, true);
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int64_t tile = tile0 + i;
+            if (i > 0) __syncthreads();   // the last tile's rows have read the window
+            park();
+            __syncthreads();
+            if (i + 1 < PT) {
+                if (++tx0 == tw) {
+                    tx0 = 0;
+                    if (++ty0 == th) {
+                        ty0 = 0;
+                        ++n0;
+                    }
+                }
+                fetch(tile + 1, true);
+            }
+            if (tile < geo.T && cg < geo.Cp)
+                input_row_groups<Elem, TT, ALPHA, P::kR, CO>(g, tab, win + c, V + tile * geo.Cp + cg,
+                                                             geo.T * geo.Cp,
+                                                             std::make_integer_sequence<int, P::kG>{});
+        }
+        return;
+    }
+    // one window: a wide layer's single tile (coordinates uniform) or a
+    // narrow layer's tiles side by side
+    if (cw == kInCh) fetch(tile0, true);
+    else fetch(tile0, false);
+    park();
+    __syncthreads();
     const int64_t tile = tile0 + (c >> cwl);
     const int64_t cg = c0 + (c & (cw - 1));
     if (tile >= geo.T || cg >= geo.Cp) return;
-    // channels C..Cp-1 read as zero and so store zeros
     input_row_groups<Elem, TT, ALPHA, P::kR, CO>(g, tab, win + c, V + tile * geo.Cp + cg, geo.T * geo.Cp,
                                                  std::make_integer_sequence<int, P::kG>{});
 }
 
-template <typename Elem, int TT, int ALPHA, bool kWhole, class CO>
+template <typename Elem, int TT, int ALPHA, bool kWhole, class CO, int PT>
 __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input_transform(
     InputTable tab, const Elem* __restrict__ x, Elem* __restrict__ V, Geometry geo) {
-    input_transform_unit<Elem, TT, ALPHA, kWhole, CO>(tab, x, V, geo, blockIdx.x, gridDim.x);
+    input_transform_unit<Elem, TT, ALPHA, kWhole, CO, PT>(tab, x, V, geo, blockIdx.x, gridDim.x);
 }
 
 // The kernel and input transforms are independent: conv2d runs them as one
 // launch.  The first n_kt workgroups each take P::kThreads runs of the kernel
 // transform, the rest are input-transform units (one launch instead of two,
 // and the short kernel transform overlaps the input transform).
-template <typename Elem, int TT, int ALPHA, bool kWhole, class CO>
+template <typename Elem, int TT, int ALPHA, bool kWhole, class CO, int PT>
 __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void kernel_input_transform(
     KernelTable ktab, InputTable itab, const Elem* __restrict__ w, const Elem* __restrict__ x,
     Elem* __restrict__ U, Elem* __restrict__ V, Geometry geo, int64_t n_kt) {
@@ -315,7 +372,7 @@ __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void kerne
         kernel_transform_run<Elem, ALPHA, 4, kWhole>(ktab, w, U, geo.K, geo.C, geo.Cp, bid * P::kThreads + threadIdx.x);
         return;
     }
-    input_transform_unit<Elem, TT, ALPHA, kWhole, CO>(itab, x, V, geo, bid - n_kt, gridDim.x - n_kt);
+    input_transform_unit<Elem, TT, ALPHA, kWhole, CO, PT>(itab, x, V, geo, bid - n_kt, gridDim.x - n_kt);
 }
 
 // ----------------------------------------------------------------- output
@@ -445,13 +502,24 @@ hipError_t launch_kernel_transform_t(const Geometry& g, const KernelTable& tab, 
 template <typename Elem, int TT, int A, class CO>
 hipError_t launch_it(const Geometry& g, const InputTable& tab, const Elem* xp, Elem* vp, hipStream_t stream) {
     constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
-    const int64_t units = input_units(g);
+    const bool whole = g.C % kChunkElems == 0;
+    // the walking instance only with compile-time coefficients (with tables
+    // read at run time its loop would hoist them all into registers)
+    constexpr bool kWalk = !__is_same(CO, RuntimeCoefs);
+    const int pt = kWalk ? input_pt(g, whole) : 1;
+    const int64_t units = input_units(g, pt);
     if (units > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(units)), block(InputShape<Elem, TT, A>::kThreads);
-    if (g.C % kChunkElems == 0)
-        hipLaunchKernelGGL((input_transform<Elem, TT, A, true, CO>), grid, block, 0, stream, tab, xp, vp, g);
+    if constexpr (kWalk)
+        if (whole && pt == kInTiles) {
+            hipLaunchKernelGGL((input_transform<Elem, TT, A, true, CO, kInTiles>), grid, block, 0, stream, tab, xp, vp,
+                               g);
+            return hipGetLastError();
+        }
+    if (whole)
+        hipLaunchKernelGGL((input_transform<Elem, TT, A, true, CO, 1>), grid, block, 0, stream, tab, xp, vp, g);
     else
-        hipLaunchKernelGGL((input_transform<Elem, TT, A, false, CO>), grid, block, 0, stream, tab, xp, vp, g);
+        hipLaunchKernelGGL((input_transform<Elem, TT, A, false, CO, 1>), grid, block, 0, stream, tab, xp, vp, g);
     return hipGetLastError();
 }
 
@@ -460,18 +528,27 @@ hipError_t launch_kit(const Geometry& g, const KernelTable& ktab, const InputTab
                       const Elem* xp, Elem* up, Elem* vp, hipStream_t stream) {
     constexpr int kChunkElems = 16 / static_cast<int>(sizeof(Elem));
     constexpr int kThr = InputShape<Elem, TT, A>::kThreads;
-    const int64_t units = input_units(g);
+    const bool whole = g.C % kChunkElems == 0;   // then C is also a multiple of the 4-channel runs
+    constexpr bool kWalk = !__is_same(CO, RuntimeCoefs);   // as in launch_it
+    const int pt = kWalk ? input_pt(g, whole) : 1;
+    const int64_t units = input_units(g, pt);
     const int64_t kt_runs = static_cast<int64_t>(g.alpha) * g.K * (g.Cp / 4);
     // a multiple of 8, so the input transform's ids keep their XCD (id mod 8)
     const int64_t n_kt = (kt_runs + 8 * kThr - 1) / (8 * kThr) * 8;
     if (n_kt + units > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(n_kt + units));
-    if (g.C % kChunkElems == 0)   // then C is also a multiple of the 4-channel runs
-        hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, true, CO>), grid, dim3(kThr), 0, stream, ktab, itab,
-                           wp, xp, up, vp, g, n_kt);
+    if constexpr (kWalk)
+        if (whole && pt == kInTiles) {
+            hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, true, CO, kInTiles>), grid, dim3(kThr), 0, stream,
+                               ktab, itab, wp, xp, up, vp, g, n_kt);
+            return hipGetLastError();
+        }
+    if (whole)
+        hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, true, CO, 1>), grid, dim3(kThr), 0, stream, ktab,
+                           itab, wp, xp, up, vp, g, n_kt);
     else
-        hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, false, CO>), grid, dim3(kThr), 0, stream, ktab, itab,
-                           wp, xp, up, vp, g, n_kt);
+        hipLaunchKernelGGL((kernel_input_transform<Elem, TT, A, false, CO, 1>), grid, dim3(kThr), 0, stream, ktab,
+                           itab, wp, xp, up, vp, g, n_kt);
     return hipGetLastError();
 }
 

@@ -46,6 +46,25 @@ def test_input_transform_bit_exact(spec, m, dtype, shape):
     assert np.all(V[:, :, C:] == 0)
 
 
+@pytest.mark.parametrize("spec,m,dtype,shape", [(WL.F4_A2P1, 4, "bf16", (3, 186, 250, 64)),
+                                                 (WL.F2_LINEAR, 2, "f16", (5, 130, 130, 128)),
+                                                 (WL.F4_A2P1, 4, "f32", (5, 130, 130, 128))])
+def test_input_transform_multi_tile_bit_exact(spec, m, dtype, shape):
+    """Layers with 8192 or more (tile, 64-channel) units run workgroups that walk
+    four tiles in turn; tile counts that are not a multiple of four leave a
+    ragged last workgroup.  Exact data: V equals the oracle bit for bit."""
+    p, op = _plan(spec, m, dtype)
+    N, H, W, C = shape
+    T = N * (-(-H // m)) * (-(-W // m))
+    assert T * (-(-C // 64)) >= 8192 and T % 4 != 0
+    dist = "ternary" if dtype == "bf16" else "int2"
+    x, _ = WL.draw_inputs(N, H, W, C, 1, dist, seed=H + W + C)
+    V = to_np(p.input_transform(to_dev(x, dtype)))
+    torch.cuda.synchronize()
+    ref = OC.input_transform_emulated(x, op, dtype).reshape(op.alpha ** 2, T, C)
+    assert np.array_equal(V[:, :, :C], ref)
+
+
 @pytest.mark.parametrize("spec,m", GENERAL)
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_input_transform_within_bound(spec, m, dtype):
