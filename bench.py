@@ -34,9 +34,11 @@ if ROOT not in sys.path:
 METRIC = "direct-equiv conv TFLOP/s + MFMA util/HBM GB/s; rel-L2 err vs fp64 direct"
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0, "bf16": 2500.0}
-KERNEL_NAMES = ("kernel_input_transform", "contract", "output_transform", "contract_output")
+KERNEL_NAMES = ("kernel_input_transform", "contract", "output_transform", "contract_output", "kernel_transform",
+                "input_contract_output")
 KERNEL_SOURCES = {"kernel_input_transform": "transforms.hip", "contract": "contract.hip",
-                  "output_transform": "transforms.hip", "contract_output": "fused.hip"}
+                  "output_transform": "transforms.hip", "contract_output": "fused.hip",
+                  "kernel_transform": "transforms.hip", "input_contract_output": "fused.hip"}
 
 
 def algorithmic_work(wl, alpha, m):
@@ -55,6 +57,10 @@ def algorithmic_work(wl, alpha, m):
         # fused: V and U in, y out, no M
         "contract_output": {"flops": 2 * a2 * T * C * K,
                             "bytes": a2 * (T * C * s + K * C * s) + wl.N * wl.H * wl.W * K * s},
+        # fused_input path: kernel transform alone, then x and U in, y out (no V, no M)
+        "kernel_transform": {"bytes": 9 * C * K * s + a2 * C * K * s},
+        "input_contract_output": {"flops": 2 * a2 * T * C * K,
+                                  "bytes": wl.N * wl.H * wl.W * C * s + a2 * K * C * s + wl.N * wl.H * wl.W * K * s},
         "T": T,
     }
 
@@ -87,7 +93,8 @@ def make_stages(plan, xd, wd, y, N_, H, W, C, K, stream):
     g = plan.geometry(N_, H, W, C, K)
     a2 = plan.alpha ** 2
     dev = xd.device
-    fused = plan.conv_path(N_, H, W, C, K) == "fused"
+    path = plan.conv_path(N_, H, W, C, K)
+    fused = path == "fused"
     U = torch.empty((a2, K, g["Cp"]), dtype=xd.dtype, device=dev)
     V = torch.empty((a2, g["T"], g["Cp"]), dtype=xd.dtype, device=dev)
     M = None if fused else torch.empty((a2, g["T"], g["Kp"]), dtype=torch.float32, device=dev)
@@ -96,6 +103,13 @@ def make_stages(plan, xd, wd, y, N_, H, W, C, K, stream):
     yt = NAT.WgTensor(ctypes.c_void_p(y.data_ptr()), N_, H, W, K)
     sh = ctypes.c_void_p(stream.cuda_stream)
     # the closures keep U, V, M and the tensor descriptors alive
+    if path == "fused_input":
+        return {
+            "kernel_transform": lambda: lib.winograd_kernel_transform(plan._h, ctypes.byref(wt),
+                                                                      ctypes.c_void_p(U.data_ptr()), sh),
+            "input_contract_output": lambda: lib.winograd_input_contract_output(
+                plan._h, ctypes.byref(xt), ctypes.c_void_p(U.data_ptr()), ctypes.byref(yt), sh),
+        }
     stages = {
         "kernel_input_transform": lambda: lib.winograd_kernel_input_transform(
             plan._h, ctypes.byref(wt), ctypes.byref(xt), ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(V.data_ptr()),
@@ -138,7 +152,7 @@ def time_kernels(stages, reps, stream):
 
 def roofline(dom, work, us, dtype):
     """Roofline record of kernel ``dom`` from its algorithmic work and time."""
-    if dom in ("contract", "contract_output"):
+    if dom in ("contract", "contract_output", "input_contract_output"):
         ai = work["flops"] / work["bytes"]
         ridge = MFMA_PEAK_TFLOPS[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
         if ai >= ridge:
@@ -210,7 +224,7 @@ def run_vgg(a):
     used = [k for k in KERNEL_NAMES if tot_us[k] > 0]
     kernels = {k: {"total_us": round(tot_us[k], 2), "algorithmic_bytes": tot_work[k]["bytes"],
                    "GB_s": round(tot_work[k]["bytes"] / (tot_us[k] * 1e-6) / 1e9, 1)} for k in used}
-    for k in ("contract", "contract_output"):
+    for k in ("contract", "contract_output", "input_contract_output"):
         if k in kernels:
             kernels[k]["TFLOP_s"] = round(tot_work[k]["flops"] / (tot_us[k] * 1e-6) / 1e12, 2)
     out = {

@@ -120,10 +120,16 @@ typedef enum { WG_FACTORS_IN_B = 0, WG_FACTORS_IN_G = 1 } wg_crt_factors;
  * WG_PATH_FUSED: one kernel contracts and applies the output transform while
  * M of each domain point is still in registers, so M never reaches memory
  * (input tiles up to 8, i.e. m <= 6, and per-plane sizes of V and U under
- * 4 GiB).  WG_PATH_AUTO picks per layer shape (winograd_conv_path reports
- * the choice).  Both paths give results within the same error bound; they
- * may differ in the last bits because the channel sums run in another order. */
-typedef enum { WG_PATH_AUTO = 0, WG_PATH_SEPARATE = 1, WG_PATH_FUSED = 2 } wg_conv_path;
+ * 4 GiB).  WG_PATH_FUSED_INPUT: the fused kernel also computes the input
+ * transform, per block into LDS, so V never reaches memory either (channel
+ * rows of at most 32 bytes, i.e. C <= 16 fp16/bf16 or C <= 8 fp32, more than
+ * 32 output channels and the block's alpha'^2 x 32 V rows within 48 KB; the
+ * same values as WG_PATH_FUSED bit for bit).  WG_PATH_AUTO picks per layer
+ * shape between the first two (winograd_conv_path reports the choice).  All
+ * paths give results within the same error bound; the separate and fused
+ * ones may differ in the last bits because the channel sums run in another
+ * order. */
+typedef enum { WG_PATH_AUTO = 0, WG_PATH_SEPARATE = 1, WG_PATH_FUSED = 2, WG_PATH_FUSED_INPUT = 3 } wg_conv_path;
 
 /* generic_transforms = 1 keeps a plan on the transform kernels that read its
  * coefficients at run time even when its tables equal a built-in plan's (see
@@ -173,9 +179,9 @@ wg_status winograd_plan_ratio(wg_plan plan, int64_t* num, int64_t* den);
 wg_status winograd_workspace_bytes(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C,
                                    int64_t K, size_t* bytes);
 
-/* The path winograd_conv2d takes for this layer shape: WG_PATH_SEPARATE or
- * WG_PATH_FUSED.  WG_ERR_UNSUPPORTED if the plan asks for WG_PATH_FUSED and
- * the shape does not allow it. */
+/* The path winograd_conv2d takes for this layer shape: WG_PATH_SEPARATE,
+ * WG_PATH_FUSED or WG_PATH_FUSED_INPUT.  WG_ERR_UNSUPPORTED if the plan asks
+ * for a fused path and the shape does not allow it. */
 wg_status winograd_conv_path(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C, int64_t K,
                              wg_conv_path* path);
 
@@ -186,7 +192,8 @@ wg_status winograd_plan_set_workspace(wg_plan plan, void* dev_ptr, size_t bytes)
 /* y = conv3x3(x, w) by eq. (2): launches the kernel transform, the input
  * transform, then the alpha'^2 batched channel contraction and the output
  * transform (separate path) or the fused kernel that does both (fused path)
- * on `stream`, using the bound workspace.  x is [N][H][W][C],
+ * on `stream`, using the bound workspace; on WG_PATH_FUSED_INPUT the kernel
+ * transform and the fused kernel that also computes V.  x is [N][H][W][C],
  * w is [K][3][3][C], y is [N][H][W][K]; N, H, W, C, K >= 1 (y->c = K). */
 wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
                           hipStream_t stream);
@@ -228,6 +235,14 @@ wg_status winograd_output_transform(wg_plan plan, const float* M, wg_tensor* y, 
  * for input tiles over 8 or per-plane sizes of V or U of 4 GiB or more. */
 wg_status winograd_contract_output(wg_plan plan, const void* V, const void* U, int64_t C, wg_tensor* y,
                                    hipStream_t stream);
+
+/* The fused kernel with the input transform in its prologue: y from x
+ * ([N][H][W][C]) and U, with V computed per block in LDS (the same values as
+ * winograd_input_transform) and never written to memory: the second kernel
+ * of winograd_conv2d on WG_PATH_FUSED_INPUT.  WG_ERR_UNSUPPORTED where that
+ * path is not available. */
+wg_status winograd_input_contract_output(wg_plan plan, const wg_tensor* x, const void* U, wg_tensor* y,
+                                         hipStream_t stream);
 
 /* Message describing the last error of the calling thread ("" if none). */
 const char* winograd_last_error(void);

@@ -31,7 +31,7 @@ class WgPlanOptions(ctypes.Structure):
 
 
 FACTOR_CODES = {"B": 0, "G": 1}
-PATH_CODES = {"auto": 0, "separate": 1, "fused": 2}
+PATH_CODES = {"auto": 0, "separate": 1, "fused": 2, "fused_input": 3}
 PATH_NAMES = {v: k for k, v in PATH_CODES.items()}
 
 
@@ -88,6 +88,8 @@ def lib():
         "winograd_contract": (ctypes.c_int, [P, P, P, P, i64, i64, i64, P]),
         "winograd_output_transform": (ctypes.c_int, [P, P, ctypes.POINTER(WgTensor), P]),
         "winograd_contract_output": (ctypes.c_int, [P, P, P, i64, ctypes.POINTER(WgTensor), P]),
+        "winograd_input_contract_output": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), P, ctypes.POINTER(WgTensor),
+                                                          P]),
         "winograd_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sigs.items():

@@ -117,6 +117,13 @@ bool fused_supported(int dt, const wg::Geometry& g) {
         default: return wg::contract_output_supported_t<2>(g);
     }
 }
+bool input_fused_supported(int dt, const wg::Geometry& g) {
+    switch (dt) {
+        case 0: return wg::input_contract_output_supported_t<0>(g);
+        case 1: return wg::input_contract_output_supported_t<1>(g);
+        default: return wg::input_contract_output_supported_t<2>(g);
+    }
+}
 
 // The path winograd_conv2d takes; -1 if the plan asks for the fused path and
 // the shape does not allow it.
@@ -131,8 +138,14 @@ bool fused_supported(int dt, const wg::Geometry& g) {
 // channel row fits two slices (C <= 64 fp32, C <= 128 fp16/bf16) and there
 // are at least 2^20 pairs.  The rule uses no device query, so the workspace
 // size it implies is the same on every machine.
+//
+// WG_PATH_FUSED_INPUT is taken only when asked for: on the RGB layer of the
+// VGG-16 stack it measured slower than the input-transform kernel followed by
+// the fused kernel (its prologue runs the transform with run-time
+// coefficients, serialised ahead of each block's contraction).
 int resolve_path(const wg_plan_s* p, const wg::Geometry& g) {
     const bool ok = fused_supported(p->dtype, g);
+    if (p->path == WG_PATH_FUSED_INPUT) return ok && input_fused_supported(p->dtype, g) ? WG_PATH_FUSED_INPUT : -1;
     if (p->path == WG_PATH_FUSED) return ok ? WG_PATH_FUSED : -1;
     if (p->path == WG_PATH_SEPARATE || !ok) return WG_PATH_SEPARATE;
     const int64_t row_bytes = g.Cp * wg::dtype_bytes(p->dtype);
@@ -156,10 +169,11 @@ Layout layout_for(const wg_plan_s* p, int64_t N, int64_t H, int64_t W, int64_t C
     const size_t ub = a2 * static_cast<size_t>(K) * static_cast<size_t>(L.g.Cp) * es;
     const size_t vb = a2 * static_cast<size_t>(L.g.T) * static_cast<size_t>(L.g.Cp) * es;
     const size_t mb = a2 * static_cast<size_t>(L.g.T) * static_cast<size_t>(L.g.Kp) * sizeof(float);
+    // no M on the fused paths, no V either when the input transform is fused
     L.u_off = 0;
     L.v_off = align256(ub);
-    L.m_off = L.v_off + align256(vb);
-    L.total = L.m_off + (L.path == WG_PATH_FUSED ? 0 : align256(mb));   // no M on the fused path
+    L.m_off = L.v_off + (L.path == WG_PATH_FUSED_INPUT ? 0 : align256(vb));
+    L.total = L.m_off + (L.path == WG_PATH_SEPARATE ? align256(mb) : 0);
     return L;
 }
 
@@ -228,6 +242,14 @@ hipError_t launch_co(int dt, const wg::Geometry& g, const wg::OutputTable& t, co
         case 0: return wg::launch_contract_output_t<0>(g, t, V, U, y, s);
         case 1: return wg::launch_contract_output_t<1>(g, t, V, U, y, s);
         default: return wg::launch_contract_output_t<2>(g, t, V, U, y, s);
+    }
+}
+hipError_t launch_ico(int dt, const wg::Geometry& g, const wg::InputTable& it, const wg::OutputTable& ot,
+                      const void* x, const void* U, void* y, hipStream_t s) {
+    switch (dt) {
+        case 0: return wg::launch_input_contract_output_t<0>(g, it, ot, x, U, y, s);
+        case 1: return wg::launch_input_contract_output_t<1>(g, it, ot, x, U, y, s);
+        default: return wg::launch_input_contract_output_t<2>(g, it, ot, x, U, y, s);
     }
 }
 
@@ -299,7 +321,7 @@ wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, 
         if (factors != WG_FACTORS_IN_B && factors != WG_FACTORS_IN_G)
             return fail(WG_ERR_ARG, "unknown CRT factor placement");
         const int path = opts ? static_cast<int>(opts->path) : WG_PATH_AUTO;
-        if (path != WG_PATH_AUTO && path != WG_PATH_SEPARATE && path != WG_PATH_FUSED)
+        if (path != WG_PATH_AUTO && path != WG_PATH_SEPARATE && path != WG_PATH_FUSED && path != WG_PATH_FUSED_INPUT)
             return fail(WG_ERR_ARG, "unknown convolution path");
         const int generic = opts ? opts->generic_transforms : 0;
         if (generic != 0 && generic != 1) return fail(WG_ERR_ARG, "generic_transforms must be 0 or 1");
@@ -418,6 +440,12 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
     void* V = base + L.v_off;
     auto* M = reinterpret_cast<float*>(base + L.m_off);
     const int dt = plan->dtype;
+    if (L.path == WG_PATH_FUSED_INPUT) {
+        // kernel transform, then the fused kernel computes V itself
+        if ((s = from_hip(launch_kt(dt, L.g, plan->ktab, w->data, U, stream), "kernel transform")) != WG_OK) return s;
+        return from_hip(launch_ico(dt, L.g, plan->itab, plan->otab, x->data, U, y->data, stream),
+                        "fused input transform and contraction");
+    }
     s = from_hip(launch_kit(dt, L.g, plan->ktab, plan->itab, w->data, x->data, U, V, plan->builtin, stream),
                  "kernel and input transforms");
     if (s != WG_OK) return s;
@@ -496,6 +524,21 @@ wg_status winograd_contract_output(wg_plan plan, const void* V, const void* U, i
     if (!fused_supported(plan->dtype, g))
         return fail(WG_ERR_UNSUPPORTED, "the fused kernel does not support this layer shape");
     return from_hip(launch_co(plan->dtype, g, plan->otab, V, U, y->data, stream), "fused contraction");
+}
+
+wg_status winograd_input_contract_output(wg_plan plan, const wg_tensor* x, const void* U, wg_tensor* y,
+                                         hipStream_t stream) {
+    wg_status s = check_plan(plan);
+    if (s != WG_OK) return s;
+    if ((s = check_tensor(x, "x")) != WG_OK || (s = check_tensor(y, "y")) != WG_OK) return s;
+    if (!U || !aligned16(U)) return fail(WG_ERR_ARG, "U must be a 16-byte aligned device pointer");
+    if (y->n != x->n || y->h != x->h || y->w != x->w) return fail(WG_ERR_ARG, "y must be [N][H][W][K] for x's N, H, W");
+    if (!dims_ok(x->n, x->h, x->w, x->c, y->c)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
+    const wg::Geometry g = wg::make_geometry(x->n, x->h, x->w, x->c, y->c, plan->tr.m, plan->tr.alpha);
+    if (!input_fused_supported(plan->dtype, g))
+        return fail(WG_ERR_UNSUPPORTED, "the input transform is not fused for this layer shape");
+    return from_hip(launch_ico(plan->dtype, g, plan->itab, plan->otab, x->data, U, y->data, stream),
+                    "fused input transform and contraction");
 }
 
 const char* winograd_last_error(void) { return g_last_error.c_str(); }

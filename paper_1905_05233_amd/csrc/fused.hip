@@ -25,6 +25,7 @@
 // descriptors clipped to the plane, so rows past T or K and bytes past a row
 // read as zero.
 #include <algorithm>
+#include <cstring>
 
 #include "device_common.hpp"
 #include "kernels.hpp"
@@ -107,19 +108,31 @@ __device__ __forceinline__ void lds_barrier() {
 // this wave are outstanding (gfx9 encoding; expcnt and lgkmcnt not waited on)
 constexpr int vm_wait(int n) { return (n & 0xf) | (0x7 << 4) | (0xf << 8) | (((n >> 4) & 0x3) << 14); }
 
-template <int D, int MM, int ALPHA, int WT, bool NARROW>
+// K1 (input transform in the prologue): 0 = off (V comes from HBM); else the
+// kernel computes the V rows of its 32 tiles itself, for every domain point,
+// into LDS before the loop, and K1 = xp (8 or 4) domain points per step.
+// Bytes of that buffer: alpha'^2 x 32 tiles x (128 / K1)-byte rows.
+template <int ALPHA, int K1> constexpr int k1_vbuf_bytes() { return K1 ? ALPHA * ALPHA * 32 * (128 / K1) : 16; }
+
+template <int D, int MM, int ALPHA, int WT, bool NARROW, int K1>
 __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
     const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, typename DTypeOf<D>::type* __restrict__ y,
-    OutputTable tab, Geometry geo, int kw, int n_kb, int rb, int n_slices, int xp) {
+    OutputTable tab, Geometry geo, int kw, int n_kb, int rb, int n_slices, int xp,
+    const typename DTypeOf<D>::type* __restrict__ x, InputTable itab) {
     using Elem = typename DTypeOf<D>::type;
     using S = Storage<Elem>;
+    static_assert(K1 == 0 || NARROW, "the input transform is fused only into the narrow-row variant");
     // four LDS stages (one step each, three steps in flight), separate arrays
     // so that the compiler can tell the stage being read from the ones being
-    // filled
-    __shared__ __attribute__((aligned(1024))) unsigned char st0[kStageBytes];
-    __shared__ __attribute__((aligned(1024))) unsigned char st1[kStageBytes];
-    __shared__ __attribute__((aligned(1024))) unsigned char st2[kStageBytes];
-    __shared__ __attribute__((aligned(1024))) unsigned char st3[kStageBytes];
+    // filled; with K1 they hold only the 64 channel rows (U)
+    constexpr int kSB = K1 ? 64 * kSlice : kStageBytes;
+    __shared__ __attribute__((aligned(1024))) unsigned char st0[kSB];
+    __shared__ __attribute__((aligned(1024))) unsigned char st1[kSB];
+    __shared__ __attribute__((aligned(1024))) unsigned char st2[kSB];
+    __shared__ __attribute__((aligned(1024))) unsigned char st3[kSB];
+    __shared__ __attribute__((aligned(16))) unsigned char vbuf[k1_vbuf_bytes<ALPHA, K1>()];
+    constexpr int kRB = K1 ? 128 / K1 : 16;   // bytes of a V row in vbuf
+    constexpr int kDma = K1 ? 2 : kDmaPerWave;   // DMA instructions per wave and step
 
     // XCD-aware numbering: the hardware deals consecutive workgroup ids
     // round-robin over the 8 XCDs; give each XCD a contiguous run of units, so
@@ -166,7 +179,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
     uint32_t roff[kDmaPerWave];
     bool live[kDmaPerWave], isu[kDmaPerWave];
 #pragma unroll
-    for (int j = 0; j < kDmaPerWave; ++j) {
+    for (int j = 0; j < kDma; ++j) {
         const int r8 = 8 * (wave + 4 * j);
         live[j] = r8 < rows;
         isu[j] = r8 < krows;
@@ -195,7 +208,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
             const bool in = any && q < ALPHA * ALPHA && piece < rb;
             const uint32_t pu = static_cast<uint32_t>(pxi * K * rb), pv = static_cast<uint32_t>(pxi * T * rb);
 #pragma unroll
-            for (int j = 0; j < kDmaPerWave; ++j)
+            for (int j = 0; j < kDma; ++j)
                 dma16(isu[j] ? ru : rv, st + (wave + 4 * j) * 1024,
                       live[j] && in ? roff[j] + (isu[j] ? pu : pv) : kOob);
         }
@@ -314,7 +327,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
         // the barrier makes every wave's visible and frees `nxt` (read in the
         // previous step) for the next request
         coefs();
-        __builtin_amdgcn_s_waitcnt(vm_wait(2 * kDmaPerWave));
+        __builtin_amdgcn_s_waitcnt(vm_wait(2 * kDma));
         lds_barrier();
         request(nxt);
         // the coefficients must be in registers before the LDS reads go out
@@ -354,8 +367,17 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
             const int col = (((p0 & 4) + grp) ^ swz) * 16;
             u32x4 fa = lds_read16(cur + a_row + col);
             u32x4 fb[WT];
+            if constexpr (K1 != 0) {
+                // this lane group's piece of domain point sq + i in vbuf (any
+                // piece for the groups that are masked below)
+                const int pc = (grp - (p0 & 3)) & (ppr - 1);
 #pragma unroll
-            for (int w = 0; w < WT; ++w) fb[w] = lds_read16(cur + b_row + w * 16 * kSlice + col);
+                for (int w = 0; w < WT; ++w)
+                    fb[w] = lds_read16(vbuf + ((sq + i) * 32 + wt * 16 * WT + w * 16 + l16) * kRB + pc * 16);
+            } else {
+#pragma unroll
+                for (int w = 0; w < WT; ++w) fb[w] = lds_read16(cur + b_row + w * 16 * kSlice + col);
+            }
             if (have_prev) fold();
             have_prev = true;
             coefs();   // for the fold of this domain point, in the next iteration
@@ -376,6 +398,72 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
     request(st0);
     request(st1);
     request(st2);
+    if constexpr (K1 != 0) {
+        // The V rows of this block's 32 tiles (kw = 4), every domain point,
+        // into vbuf at [q][tile][kRB bytes], q = b alpha' + a the visiting
+        // order of the loop; the first U requests are already in flight.
+        // Each (tile, channel) pair runs the input transform of eq. (2) in the
+        // order of the stand-alone kernel: pass 1 W = B^T d in ascending u,
+        // pass 2 in ascending v, fp32 fused multiply-adds from zero, rounded
+        // once to the storage type (the same values bit for bit); padding
+        // channels and tiles past T hold zeros.  Tile coordinates are carried
+        // from the block's first tile (T < 2^28 here, so 32-bit arithmetic).
+        constexpr int TT = MM + 2;
+        constexpr int kNE = kRB / static_cast<int>(sizeof(Elem));   // channels of a vbuf row
+        const int tw = static_cast<int>(geo.tw), th = static_cast<int>(geo.th);
+        const int tx0 = static_cast<int>(t0 % geo.tw);
+        const int ty0 = static_cast<int>((t0 / geo.tw) % geo.th);
+        const int n0 = static_cast<int>(t0 / (geo.tw * geo.th));
+        const int H = static_cast<int>(geo.H), Wd = static_cast<int>(geo.W), C = static_cast<int>(geo.C);
+        for (int pr = tid; pr < 32 * kNE; pr += kThreads) {
+            const int r = pr / kNE, c = pr % kNE;
+            int tx = tx0 + r, ty = ty0, n = n0;
+            while (tx >= tw) {
+                tx -= tw;
+                if (++ty == th) {
+                    ty = 0;
+                    ++n;
+                }
+            }
+            const bool live_t = t0 + r < T && c < C;
+            float d[TT][TT];
+#pragma unroll
+            for (int u = 0; u < TT; ++u) {
+                const int hr = ty * geo.m - 1 + u;
+                const int wc0 = tx * geo.m - 1;
+                const Elem* row = x + ((static_cast<int64_t>(n) * H + hr) * Wd + wc0) * C + c;
+#pragma unroll
+                for (int v = 0; v < TT; ++v) {
+                    const bool in = live_t && hr >= 0 && hr < H && wc0 + v >= 0 && wc0 + v < Wd;
+                    d[u][v] = in ? S::to_f32(row[v * C]) : 0.0f;
+                }
+            }
+#pragma unroll
+            for (int a = 0; a < ALPHA; ++a) {
+                float w1[TT];
+#pragma unroll
+                for (int v = 0; v < TT; ++v) {
+                    float acc = 0.0f;
+#pragma unroll
+                    for (int u = 0; u < TT; ++u) acc = __builtin_fmaf(itab.bt[a * TT + u], d[u][v], acc);
+                    w1[v] = acc;
+                }
+#pragma unroll
+                for (int b = 0; b < ALPHA; ++b) {
+                    float acc = 0.0f;
+#pragma unroll
+                    for (int v = 0; v < TT; ++v) acc = __builtin_fmaf(itab.bt[b * TT + v], w1[v], acc);
+                    *reinterpret_cast<Elem*>(vbuf + ((b * ALPHA + a) * 32 + r) * kRB + c * sizeof(Elem)) =
+                        S::from_f32(acc);
+                }
+            }
+        }
+        // this wave's vbuf writes done, then every wave's (no wait for the
+        // U requests in flight)
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        lds_barrier();
+    }
+
     // step s reads stage s % 4 and requests step s + 3 into stage (s + 3) % 4
     for (int s0 = 0; s0 < nsteps; s0 += 4) {
         step(st0, st3);
@@ -443,12 +531,50 @@ bool contract_output_supported_t<WG_DTYPE>(const Geometry& g) {
     return g.T * rb < 0xffff0000LL && g.K * rb < 0xffff0000LL && rb <= (1 << 20);
 }
 
+// the input transform fused into the prologue: rows of at most 32 bytes (8 or
+// 4 domain points per step), more than 32 output channels (so a block has
+// 32 tiles whatever its shape) and the block's V rows within 48 KB of LDS (two
+// workgroups per CU)
 template <>
-hipError_t launch_contract_output_t<WG_DTYPE>(const Geometry& g, const OutputTable& tab, const void* V,
-                                              const void* U, void* y, hipStream_t stream) {
-    constexpr int D = WG_DTYPE;
+bool input_contract_output_supported_t<WG_DTYPE>(const Geometry& g) {
+    const int64_t rb = g.Cp * (WG_DTYPE == 0 ? 4 : 2);
+    const int64_t a2 = static_cast<int64_t>(g.alpha) * g.alpha;
+    if (!contract_output_supported_t<WG_DTYPE>(g) || rb > 32 || g.K <= 32) return false;
+    const int64_t vrow = rb <= 16 ? 16 : 32;
+    return a2 * g.K * rb < 0xffff0000LL && a2 * 32 * vrow <= 49152;
+}
+
+namespace {
+
+struct CoArgs {
+    const unsigned char* V;
+    const unsigned char* U;
+    void* y;
+    OutputTable tab;
+    Geometry g;
+    int kw, n_kb, rb, n_slices, xp;
+    const void* x;
+    InputTable itab;
+    unsigned nb;
+};
+
+template <int D, int TT, int A, int W, bool NAR, int K1>
+hipError_t launch_co_instance(const CoArgs& c, hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
-    if (!contract_output_supported_t<D>(g)) return hipErrorInvalidValue;
+    if constexpr (k1_vbuf_bytes<A, K1>() <= 49152) {
+        hipLaunchKernelGGL((contract_output_kernel<D, TT - 2, A, W, NAR, K1>), dim3(c.nb), dim3(kThreads), 0, stream,
+                           c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.kw, c.n_kb, c.rb, c.n_slices, c.xp,
+                           static_cast<const Elem*>(c.x), c.itab);
+        return hipGetLastError();
+    } else {
+        return hipErrorInvalidValue;
+    }
+}
+
+// x == nullptr: V from memory; else the input transform in the prologue
+template <int D>
+hipError_t launch_co(const Geometry& g, const OutputTable& tab, const void* V, const void* U, void* y,
+                     const void* x, const InputTable* itab, hipStream_t stream) {
     const int rb = static_cast<int>(g.Cp * (D == 0 ? 4 : 2));
     const int kw0 = g.K <= 16 ? 1 : g.K <= 32 ? 2 : 4;
     const int wt = pick_wt(g, std::max(kw0, 2));
@@ -461,19 +587,30 @@ hipError_t launch_contract_output_t<WG_DTYPE>(const Geometry& g, const OutputTab
     // addressed with 32-bit offsets); else one 128-byte slice per step
     int xp = 1;
     const int64_t a2 = static_cast<int64_t>(g.alpha) * g.alpha;
-    if (rb <= 64 && a2 * g.T * rb < 0xffff0000LL && a2 * g.K * rb < 0xffff0000LL) xp = rb <= 16 ? 8 : rb <= 32 ? 4 : 2;
-    const int n_slices = xp > 1 ? 1 : (rb + kSlice - 1) / kSlice;
-    const auto* vp = static_cast<const unsigned char*>(V);
-    const auto* up = static_cast<const unsigned char*>(U);
-    auto* yp = static_cast<Elem*>(y);
-    const unsigned nb = static_cast<unsigned>(grid);
-#define WG_CO_LAUNCH(TT, A, W, NAR)                                                                       \
-    hipLaunchKernelGGL((contract_output_kernel<D, TT - 2, A, W, NAR>), dim3(nb), dim3(kThreads), 0, stream, vp, \
-                       up, yp, tab, g, kw, n_kb, rb, n_slices, xp);
+    if (x) xp = rb <= 16 ? 8 : 4;   // checked by input_contract_output_supported_t
+    else if (rb <= 64 && a2 * g.T * rb < 0xffff0000LL && a2 * g.K * rb < 0xffff0000LL)
+        xp = rb <= 16 ? 8 : rb <= 32 ? 4 : 2;
+    CoArgs c;
+    c.V = static_cast<const unsigned char*>(x ? U : V);   // unused with the input transform fused
+    c.U = static_cast<const unsigned char*>(U);
+    c.y = y;
+    c.tab = tab;
+    c.g = g;
+    c.kw = kw;
+    c.n_kb = n_kb;
+    c.rb = rb;
+    c.n_slices = xp > 1 ? 1 : (rb + kSlice - 1) / kSlice;
+    c.xp = xp;
+    c.x = x;
+    if (itab) c.itab = *itab;
+    else std::memset(&c.itab, 0, sizeof(c.itab));
+    c.nb = static_cast<unsigned>(grid);
 #define WG_CO_CASE(TT, A, W)                                                                              \
     if (g.t == TT && g.alpha == A && wt == W) {                                                           \
-        if (xp > 1) WG_CO_LAUNCH(TT, A, W, true) else WG_CO_LAUNCH(TT, A, W, false)                       \
-        return hipGetLastError();                                                                         \
+        if (x && xp == 8) return launch_co_instance<D, TT, A, W, true, 8>(c, stream);                     \
+        if (x) return launch_co_instance<D, TT, A, W, true, 4>(c, stream);                                \
+        if (xp > 1) return launch_co_instance<D, TT, A, W, true, 0>(c, stream);                           \
+        return launch_co_instance<D, TT, A, W, false, 0>(c, stream);                                      \
     }
     WG_CO_CASE(4, 4, 1) WG_CO_CASE(4, 5, 1) WG_CO_CASE(4, 6, 1) WG_CO_CASE(4, 7, 1)
     WG_CO_CASE(4, 4, 2) WG_CO_CASE(4, 5, 2) WG_CO_CASE(4, 6, 2) WG_CO_CASE(4, 7, 2)
@@ -481,8 +618,24 @@ hipError_t launch_contract_output_t<WG_DTYPE>(const Geometry& g, const OutputTab
     WG_CO_CASE(6, 6, 2) WG_CO_CASE(6, 7, 2) WG_CO_CASE(6, 8, 2) WG_CO_CASE(6, 9, 2)
     WG_CO_CASE(8, 8, 1) WG_CO_CASE(8, 9, 1) WG_CO_CASE(8, 10, 1) WG_CO_CASE(8, 11, 1) WG_CO_CASE(8, 12, 1)
 #undef WG_CO_CASE
-#undef WG_CO_LAUNCH
     return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+template <>
+hipError_t launch_contract_output_t<WG_DTYPE>(const Geometry& g, const OutputTable& tab, const void* V,
+                                              const void* U, void* y, hipStream_t stream) {
+    if (!contract_output_supported_t<WG_DTYPE>(g)) return hipErrorInvalidValue;
+    return launch_co<WG_DTYPE>(g, tab, V, U, y, nullptr, nullptr, stream);
+}
+
+template <>
+hipError_t launch_input_contract_output_t<WG_DTYPE>(const Geometry& g, const InputTable& itab,
+                                                    const OutputTable& otab, const void* x, const void* U, void* y,
+                                                    hipStream_t stream) {
+    if (!input_contract_output_supported_t<WG_DTYPE>(g) || !x) return hipErrorInvalidValue;
+    return launch_co<WG_DTYPE>(g, otab, nullptr, U, y, x, &itab, stream);
 }
 
 }  // namespace wg

@@ -135,7 +135,7 @@ class Plan:
         return out.value
 
     def conv_path(self, N_, H, W, C, K):
-        """"separate" or "fused": the path conv2d takes for this layer shape."""
+        """"separate", "fused" or "fused_input": the path conv2d takes for this layer shape."""
         out = ctypes.c_int()
         N.check(self._lib.winograd_conv_path(self._h, N_, H, W, C, K, ctypes.byref(out)))
         return N.PATH_NAMES[out.value]
@@ -281,6 +281,21 @@ class Plan:
         N.check(self._lib.winograd_contract_output(self._h, ctypes.c_void_p(V.data_ptr()),
                                                    ctypes.c_void_p(U.data_ptr()), C, ctypes.byref(yt),
                                                    _stream_handle(stream)))
+        return y
+
+    def input_contract_output(self, x, U, stream=None):
+        """The fused kernel with the input transform in its prologue: y [N][H][W][K]
+        from x and U, neither V nor M in memory."""
+        self._check_dtype(x, "x")
+        self._check_dtype(U, "U")
+        Nn, H, W, C = x.shape
+        a2, K, Cp = U.shape
+        if a2 != self.alpha ** 2 or Cp != -(-C // 8) * 8 or not U.is_contiguous():
+            raise ValueError("U must be a contiguous [alpha'^2][K][Cp] tensor for x's C")
+        y = torch.empty((Nn, H, W, K), dtype=self.torch_dtype, device=x.device)
+        xt, yt = _tensor(x, "x"), _tensor(y, "y")
+        N.check(self._lib.winograd_input_contract_output(self._h, ctypes.byref(xt), ctypes.c_void_p(U.data_ptr()),
+                                                         ctypes.byref(yt), _stream_handle(stream)))
         return y
 
     # ------------------------------------------------------------ lifetime

@@ -190,6 +190,31 @@ def test_conv_path_option_and_workspace():
         Plan(WL.F4_LINEAR, m=4, path="fast")
 
 
+def test_fused_input_path_rule():
+    """WG_PATH_FUSED_INPUT (the input transform inside the fused kernel) is taken
+    only when asked for, on channel rows of at most 32 bytes, more than 32
+    output channels and alpha'^2 x 32 V rows within 48 KB; it needs neither V
+    nor M in the workspace."""
+    vgg0 = (32, 224, 224, 3, 64)
+    ok = [(WL.F4_A2P1, 4, "bf16"), (WL.F4_A2P1, 4, "f16"), (WL.F6_LINEAR, 6, "bf16"), (WL.F4_LINEAR, 4, "f32")]
+    for spec, m, dt in ok:
+        assert Plan(spec, m=m, dtype=dt, path="fused_input").conv_path(*vgg0) == "fused_input"
+        assert Plan(spec, m=m, dtype=dt).conv_path(*vgg0) == "fused"          # never chosen automatically
+    no = [(WL.F4_A2P1, 4, "f32", vgg0),                       # 32-byte rows, alpha' 7: 49 KB of V rows
+          (WL.F6_TWO_QUAD, 6, "bf16", vgg0),                  # alpha' 10: 50 KB
+          (WL.F4_A2P1, 4, "bf16", (32, 224, 224, 3, 32)),     # K <= 32
+          (WL.F4_A2P1, 4, "bf16", (32, 224, 224, 24, 64))]    # 48-byte rows
+    for spec, m, dt, shape in no:
+        with pytest.raises(N.WinogradError) as ei:
+            Plan(spec, m=m, dtype=dt, path="fused_input").conv_path(*shape)
+        assert ei.value.status == 5
+    pf, pi = Plan(WL.F4_A2P1, m=4, dtype="bf16", path="fused"), Plan(WL.F4_A2P1, m=4, dtype="bf16", path="fused_input")
+    Nn, H, W, C, K = 1, 9, 9, 3, 40
+    T = Nn * 3 * 3
+    v_bytes = -(-49 * T * 8 * 2 // 256) * 256
+    assert pf.workspace_bytes(Nn, H, W, C, K) - pi.workspace_bytes(Nn, H, W, C, K) == v_bytes
+
+
 def test_workspace_bytes_and_errors():
     p = Plan(WL.F4_LINEAR, m=4, dtype="f32", path="separate")
     Nn, H, W, C, K = 8, 56, 56, 128, 128

@@ -140,3 +140,66 @@ def test_fused_unsupported_shape_raises():
     x, w = _inputs((1, 16, 16, 8, 8), "f32", seed=1)
     with pytest.raises(WinogradError, match="UNSUPPORTED"):
         p.conv2d(to_dev(x, "f32"), to_dev(w, "f32"))
+
+
+# layers whose fused kernel also computes V (rows of at most 32 bytes, K > 32)
+FUSE_INPUT = [
+    (WL.F2_LINEAR, 2, "f32", (2, 26, 30, 3, 40)),        # 32-byte rows: 4 domain points per step
+    (WL.F4_LINEAR, 4, "f32", (1, 19, 17, 8, 70)),
+    (WL.F4_A2P1, 4, "bf16", (2, 26, 30, 3, 40)),         # 16-byte rows: 8 per step
+    (WL.F4_A2P1, 4, "f16", (1, 19, 17, 8, 70)),
+    (WL.F6_LINEAR, 6, "bf16", (2, 23, 29, 5, 96)),
+    (WL.F4_LINEAR, 4, "bf16", (1, 21, 22, 16, 48)),      # 32-byte rows in 16-bit storage
+]
+
+
+@pytest.mark.parametrize("spec,m,dtype,shape", FUSE_INPUT,
+                         ids=[f"{s}-m{m}-{d}-{sh}" for s, m, d, sh in FUSE_INPUT])
+def test_fused_input_transform(spec, m, dtype, shape):
+    """The input transform in the fused kernel's prologue gives the same bits as
+    the input-transform kernel followed by the fused kernel, and conv2d on the
+    fused_input path is that kernel; against the oracle, the 2x rule and the
+    bound."""
+    N, H, W, C, K = shape
+    print(f"[fused-input] {spec} m={m} {dtype} {shape}", flush=True)
+    x, w = _inputs(shape, dtype, seed=m + C + K)
+    p = _plan(spec, m, dtype, "fused_input")
+    assert p.conv_path(N, H, W, C, K) == "fused_input"
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
+    U = p.kernel_transform(wd)
+    y_two = p.contract_output(p.input_transform(xd), U, C, N, H, W)
+    y_one = p.input_contract_output(xd, U)
+    y_conv = p.conv2d(xd, wd)
+    torch.cuda.synchronize()
+    assert torch.equal(y_one, y_two)
+    assert torch.equal(y_conv, y_two)
+    y = to_np(y_conv).astype(np.float64)
+    op = OP.build_plan(spec, n_o=m)
+    y64 = OC.direct_f64(x, w)
+    yo = OC.winograd_emulated(x, w, op, dtype)
+    assert OC.rel_l2(y, y64) <= 2 * OC.rel_l2(yo, y64)
+    bound = elementwise_bound(x, w, op, dtype, y64)
+    assert np.all(np.abs(y - y64) <= bound)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+def test_fused_input_transform_bit_exact_dyadic(dtype):
+    """Small integers through a dyadic plan: every rounding exact, so the
+    fused-input kernel equals direct convolution bit for bit."""
+    N, H, W, C, K = 2, 30, 27, 3, 64
+    dist = "ternary" if dtype == "bf16" else "int2"
+    x, w = WL.draw_inputs(N, H, W, C, K, dist, seed=17)
+    spec, m = (WL.F2_LINEAR, 2) if dtype == "f32" else (WL.F4_A2P1, 4)
+    p = _plan(spec, m, dtype, "fused_input")
+    assert p.conv_path(N, H, W, C, K) == "fused_input"
+    y = to_np(p.conv2d(to_dev(x, dtype), to_dev(w, dtype))).astype(np.float64)
+    assert np.array_equal(y, OC.direct_f64(x, w))
+
+
+def test_fused_input_transform_unsupported_raises():
+    from paper_1905_05233_amd._native import WinogradError
+    p = _plan(WL.F4_A2P1, 4, "bf16", "fused")
+    x, w = _inputs((1, 16, 16, 24, 64), "bf16", seed=2)       # 48-byte rows
+    U = p.kernel_transform(to_dev(w, "bf16"))
+    with pytest.raises(WinogradError, match="UNSUPPORTED"):
+        p.input_contract_output(to_dev(x, "bf16"), U)
