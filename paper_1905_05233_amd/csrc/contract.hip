@@ -89,28 +89,33 @@ __global__ __launch_bounds__(kThreads, 2) void contract_kernel(const unsigned ch
     const int half = lane >> 5;
     const int r32 = lane & 31;
 
-    // global -> register staging: 4 chunks of A and 4 of B per thread
+    // global -> register staging: 4 chunks of A and 4 of B per thread, in two
+    // register sets, so that two k-tiles are in flight while one is computed
     const int lrow = tid >> 3;          // 0..31, + 32 p
     const int lcol = tid & 7;
-    u32x4 ra[4], rb[4];
-    const u32x4 zero = {0u, 0u, 0u, 0u};
+    u32x4 ra[2][4], rb[2][4];
+    // buffer descriptors over the block's own rows: rows past T or K and
+    // bytes past the row read zero, with no branch (a branch per load would
+    // make the compiler wait for every load in flight where the paths join);
+    // the launcher checks that 128 rows stay below the out-of-range offset
+    const auto rv = make_rsrc(Vb + m0 * row_bytes, (T - m0 < kBM ? T - m0 : kBM) * row_bytes);
+    const auto ru = make_rsrc(Ub + n0 * row_bytes, (K - n0 < kBN ? K - n0 : kBN) * row_bytes);
 
-    auto gload = [&](int kt) {
+    auto gload = [&](int set, int kt) __attribute__((always_inline)) {
         const int64_t byte = static_cast<int64_t>(kt) * (kRowChunks * 16) + lcol * 16;
         const bool kin = byte < row_bytes;  // row_bytes is a multiple of 16
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
-            const int64_t gm = m0 + lrow + 32 * p;
-            const int64_t gn = n0 + lrow + 32 * p;
-            ra[p] = (kin && gm < T) ? *reinterpret_cast<const u32x4*>(Vb + gm * row_bytes + byte) : zero;
-            rb[p] = (kin && gn < K) ? *reinterpret_cast<const u32x4*>(Ub + gn * row_bytes + byte) : zero;
+            const uint32_t off = static_cast<uint32_t>((lrow + 32 * p) * row_bytes + byte);
+            ra[set][p] = __builtin_amdgcn_raw_buffer_load_b128(rv, kin ? off : kOob, 0, 0);
+            rb[set][p] = __builtin_amdgcn_raw_buffer_load_b128(ru, kin ? off : kOob, 0, 0);
         }
     };
-    auto sstore = [&](int buf) {
+    auto sstore = [&](int set, int buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
-            lds[buf][(lrow + 32 * p) * kLdsChunks + lcol] = ra[p];
-            lds[buf][(kBM + lrow + 32 * p) * kLdsChunks + lcol] = rb[p];
+            lds[buf][(lrow + 32 * p) * kLdsChunks + lcol] = ra[set][p];
+            lds[buf][(kBM + lrow + 32 * p) * kLdsChunks + lcol] = rb[set][p];
         }
     };
 
@@ -123,12 +128,9 @@ __global__ __launch_bounds__(kThreads, 2) void contract_kernel(const unsigned ch
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     const int nk = static_cast<int>((row_bytes + kRowChunks * 16 - 1) / (kRowChunks * 16));
-    gload(0);
-    sstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) gload(kt + 1);
+    // k-tile kt is loaded into register set kt % 2 two k-tiles ahead and
+    // parked in LDS buffer kt % 2 one k-tile ahead
+    auto compute = [&](int buf) __attribute__((always_inline)) {
         const u32x4* L = lds[buf];
         const int arow0 = (wm * 64 + r32) * kLdsChunks;
         const int arow1 = (wm * 64 + 32 + r32) * kLdsChunks;
@@ -146,7 +148,25 @@ __global__ __launch_bounds__(kThreads, 2) void contract_kernel(const unsigned ch
             mma_chunk<D>(a1, b0, acc[1][0]);
             mma_chunk<D>(a1, b1, acc[1][1]);
         }
-        if (kt + 1 < nk) sstore(buf ^ 1);
+    };
+    // the loads are issued unconditionally (k-tiles past the row read zero):
+    // a load behind a branch would make the compiler drain every load in
+    // flight where the paths join
+    gload(0, 0);
+    gload(1, 1);
+    sstore(0, 0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+        // even k-tile: computed from buffer 0, its set refilled with kt + 2
+        gload(0, kt + 2);
+        compute(0);
+        if (kt + 1 < nk) sstore(1, 1);
+        __syncthreads();
+        if (kt + 1 >= nk) break;
+        // odd k-tile: buffer 1, set 1 refilled with kt + 3
+        gload(1, kt + 3);
+        compute(1);
+        if (kt + 2 < nk) sstore(0, 0);
         __syncthreads();
     }
 
@@ -472,7 +492,8 @@ hipError_t launch_contract_t(const Geometry& g, const void* V, const void* U, fl
     const int num_mb = static_cast<int>((g.T + kBM - 1) / kBM);
     const int num_nb = static_cast<int>((g.K + kBN - 1) / kBN);
     const int64_t blocks = static_cast<int64_t>(num_mb) * num_nb * g.alpha * g.alpha;
-    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    // the block kernel addresses its 128 rows of V and of U with 32-bit offsets
+    if (blocks > 0x7fffffff || std::max(kBM, kBN) * row_bytes >= 0xffff0000LL) return hipErrorInvalidValue;
     hipLaunchKernelGGL(contract_kernel<D>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream,
                        static_cast<const unsigned char*>(V), static_cast<const unsigned char*>(U), M, g.T, g.K,
                        row_bytes, g.Kp, num_mb, num_nb);

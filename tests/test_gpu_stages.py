@@ -104,7 +104,8 @@ def test_kernel_transform(spec, m, dtype):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("T,C,K", [(1, 1, 1), (37, 8, 5), (129, 40, 130), (300, 264, 96), (1568, 128, 128)])
+@pytest.mark.parametrize("T,C,K", [(1, 1, 1), (37, 8, 5), (129, 40, 130), (300, 264, 96), (130, 320, 257),
+                                   (1568, 128, 128)])
 def test_contract_bit_exact_on_integers(dtype, T, C, K):
     p, _ = _plan(WL.F4_A2P1, 4, dtype)
     a2 = p.alpha ** 2
