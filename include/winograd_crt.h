@@ -222,7 +222,11 @@ wg_status winograd_kernel_input_transform(wg_plan plan, const wg_tensor* w, cons
 
 /* M[xi][t][k] = sum_c V[xi][t][c] U[xi][k][c]: alpha'^2 GEMMs [T x C][C x K]
  * on the matrix cores with fp32 accumulation (the Hadamard product of eq. (2)
- * summed over input channels). */
+ * summed over input channels).  The kernels address 128 rows of V or U with
+ * 32-bit offsets: a channel row (Cp storage elements) of 33,553,920 bytes
+ * (just under 32 MiB) or more, or
+ * more than 2^31 - 1 blocks of 128 x 128, fails with WG_ERR_HIP ("invalid
+ * argument") before anything is launched. */
 wg_status winograd_contract(wg_plan plan, const void* V, const void* U, float* M, int64_t T,
                             int64_t C, int64_t K, hipStream_t stream);
 
