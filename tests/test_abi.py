@@ -250,6 +250,17 @@ def test_unsupported_kernel_shape_reported_at_launch():
     assert lib.winograd_input_transform(p._h, ctypes.byref(x), fake, None) == 5
 
 
+def test_contraction_row_limit_reported_before_launch():
+    """Channel rows too long for the kernels' 32-bit offsets (128 rows of
+    36 MB here) fail with WG_ERR_HIP before anything is launched; the pointers
+    are never dereferenced."""
+    p = Plan(WL.F4_LINEAR, m=4, dtype="f32", path="separate")
+    lib = N.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    st = lib.winograd_contract(p._h, fake, fake, fake, 1, 9_000_000, 1, None)
+    assert st == 8 and b"contraction" in lib.winograd_last_error()
+
+
 def test_geometry_helpers():
     p = Plan(WL.F6_LINEAR, m=6, dtype="bf16")
     g = p.geometry(16, 28, 28, 256, 256)
