@@ -20,8 +20,9 @@ Functions:
 * ``winograd_exact``    eq. (2) tile by tile in exact rationals (tiny inputs);
 * ``winograd_emulated`` eq. (2) with the rounding points of the GPU library:
   matrices rounded once to fp32; B^T d B and G g G^T as two 1D passes in fp32
-  with ascending-index sums, then rounded to the storage dtype; the channel
-  sum in fp32 of storage-dtype products; A^T M A in fp32, rounded to the dtype;
+  with ascending-index sums of fused multiply-adds (one rounding per term),
+  then rounded to the storage dtype; the channel sum in fp32 of
+  storage-dtype products; A^T M A as two such passes, rounded to the dtype;
 * ``abs_bound``         the magnitude sum |A^T| sum_c (|G||g||G^T|) (.)
   (|B^T||d||B|) |A| that bounds every rounding error of the algorithm;
 * ``rel_l2``            ||y - y_ref||_2 / ||y_ref||_2 in float64.
@@ -171,13 +172,14 @@ def plan_f32(plan):
 
 
 def _left(Mt, d, axis):
-    """out[..., i, ...] = sum_k Mt[i, k] * d[..., k, ...], fp32, ascending k."""
+    """out[..., i, ...] = sum_k Mt[i, k] * d[..., k, ...] in fp32: from zero,
+    ascending k, each term added by one fused multiply-add (one rounding)."""
     d = np.moveaxis(d, axis, 0)
     out = np.empty((Mt.shape[0],) + d.shape[1:], dtype=np.float32)
     for i in range(Mt.shape[0]):
         acc = np.zeros(d.shape[1:], dtype=np.float32)
         for k in range(Mt.shape[1]):
-            acc = acc + Mt[i, k] * d[k]
+            acc = fp.fma_f32(Mt[i, k], d[k], acc)
         out[i] = acc
     return np.moveaxis(out, 0, axis)
 
@@ -230,8 +232,10 @@ def output_transform_emulated(M, plan, dtype, H, W, mats=None):
     return np.ascontiguousarray(y[:, :H, :W, :])
 
 
-def winograd_emulated(x, w, plan, dtype):
-    """Full layer by eq. (2) with the library's rounding points (see module doc).
+def winograd_emulated_stages(x, w, plan, dtype):
+    """Full layer by eq. (2) with the library's rounding points (see module
+    doc), returning every stage: U [al][al][K][C], V [al][al][N][th][tw][C],
+    M [al][al][N][th][tw][K] (fp32) and y [N][H][W][K].
 
     ``x`` and ``w`` must already hold values representable in ``dtype``.
     """
@@ -242,7 +246,13 @@ def winograd_emulated(x, w, plan, dtype):
     U = kernel_transform_emulated(w, plan, dtype, mats)
     V = input_transform_emulated(x, plan, dtype, mats)
     M = contraction_emulated(V, U)
-    return output_transform_emulated(M, plan, dtype, x.shape[1], x.shape[2], mats)
+    y = output_transform_emulated(M, plan, dtype, x.shape[1], x.shape[2], mats)
+    return {"U": U, "V": V, "M": M, "y": y}
+
+
+def winograd_emulated(x, w, plan, dtype):
+    """Full layer by eq. (2) with the library's rounding points; y only."""
+    return winograd_emulated_stages(x, w, plan, dtype)["y"]
 
 
 # ---------------------------------------------------------------------------

@@ -81,3 +81,35 @@ def to_dtype(x, dtype):
     if dtype == "bf16":
         return round_bf16(x)
     raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def fma_f32(a, b, c):
+    """a * b + c rounded once to fp32 (round to nearest even), elementwise.
+
+    The transforms of the library accumulate each term with one fused
+    multiply-add, so the emulation rounds a product and its sum together.
+    The product of two fp32 values is exact in float64 (48 significant bits);
+    the float64 sum s = p + c is then exact up to the error e that TwoSum
+    recovers.  Rounding s to fp32 gives the correctly rounded p + c unless s
+    lies exactly half-way between two fp32 numbers while e is not zero (a
+    double rounding); then the exact sum p + c lies on e's side of that
+    midpoint and rounds to the neighbour there.
+    """
+    a = np.asarray(a, dtype=np.float32)
+    b = np.asarray(b, dtype=np.float32)
+    c = np.asarray(c, dtype=np.float32)
+    p = a.astype(np.float64) * b.astype(np.float64)
+    c64 = c.astype(np.float64)
+    s = p + c64
+    bv = s - p
+    e = (p - (s - bv)) + (c64 - bv)                  # TwoSum: p + c == s + e exactly
+    with np.errstate(over="ignore", invalid="ignore"):
+        r = s.astype(np.float32)
+        r64 = r.astype(np.float64)
+        other = np.nextafter(r, np.where(s > r64, np.float32(np.inf), np.float32(-np.inf)).astype(np.float32))
+        mid = (r64 + other.astype(np.float64)) * 0.5
+        tie = (s != r64) & (s == mid) & (e != 0)
+        up = np.maximum(r, other)
+        down = np.minimum(r, other)
+        out = np.where(tie, np.where(e > 0, up, down), r)
+    return out.astype(np.float32)

@@ -75,3 +75,30 @@ def test_fraction_to_f32_ties_to_even():
 @pytest.mark.parametrize("q", [Fraction(1, 2), Fraction(-5, 4), Fraction(3), Fraction(0)])
 def test_fraction_to_f32_exact_values(q):
     assert OF.fraction_to_f32(q) == float(q)
+
+
+def test_fma_f32_is_correctly_rounded():
+    """fma_f32 against the exact rational a*b + c rounded once by
+    fraction_to_f32 (itself pinned by brute force above), on random triples of
+    spread exponents, on cancelling triples (c close to -a*b), and on a triple
+    whose float64 sum lands exactly half-way between two fp32 numbers while
+    the exact sum does not (a naive double rounding picks the wrong side)."""
+    rng = np.random.default_rng(11)
+    n = 4000
+    a = (rng.standard_normal(n) * 2.0 ** rng.integers(-20, 20, n)).astype(np.float32)
+    b = (rng.standard_normal(n) * 2.0 ** rng.integers(-20, 20, n)).astype(np.float32)
+    c = (rng.standard_normal(n) * 2.0 ** rng.integers(-40, 40, n)).astype(np.float32)
+    cancel = rng.random(n) < 0.3
+    c[cancel] = (-(a[cancel].astype(np.float64) * b[cancel].astype(np.float64))).astype(np.float32)
+    got = OF.fma_f32(a, b, c)
+    for i in range(n):
+        exact = Fraction(float(a[i])) * Fraction(float(b[i])) + Fraction(float(c[i]))
+        assert float(got[i]) == OF.fraction_to_f32(exact), i
+    # p = 2^-24 (1 + 2^-23)(1 - 2^-23) = 2^-24 - 2^-70 and c = 1 + 2^-23: the
+    # float64 sum is the midpoint 1 + 2^-23 + 2^-24; the exact sum is just below
+    a1 = np.float32(2.0 ** -24 * (1 + 2.0 ** -23))
+    b1 = np.float32(1 - 2.0 ** -23)
+    c1 = np.float32(1 + 2.0 ** -23)
+    naive = np.float32(np.float64(a1) * np.float64(b1) + np.float64(c1))
+    assert float(naive) == 1 + 2.0 ** -22
+    assert float(OF.fma_f32(a1, b1, c1)) == 1 + 2.0 ** -23

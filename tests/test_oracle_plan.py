@@ -283,3 +283,81 @@ def test_factors_in_g_move_exactly_the_crt_factors(spec, m, inner):
                     for i in range(rows)]
             assert pg.G[x:x + rows] == want
         x += rows
+
+
+# ---------------------------------------------------------------------------
+# The exact checkers must see a broken plan (values computed by hand)
+# ---------------------------------------------------------------------------
+
+def _f23():
+    """F(2x2) on {0, 1, -1, inf}: G = [[1,0,0],[1,1,1],[1,-1,1],[0,0,1]],
+    A = [[1,0],[1,1],[1,-1],[0,1]], B^T = [[1,0,-1,0],[0,1/2,1/2,0],
+    [0,-1/2,1/2,0],[0,-1,0,1]] (Algorithms 1 and 2)."""
+    import copy
+    return copy.deepcopy(OP.build_plan("0,1,-1,inf", n_o=2))
+
+
+def test_trilinear_defect_sees_a_perturbed_g_entry():
+    """G[1][2] += 1/2 changes sum_xi B[k,xi] G[xi,2] A[xi,j] by
+    B[k,1] * 1/2 * A[1,j]; the largest such change is (1/2)(1/2)(1) = 1/4."""
+    pl = _f23()
+    assert OP.trilinear_defect(pl) == 0
+    pl.G[1][2] += Fraction(1, 2)
+    assert OP.trilinear_defect(pl) == Fraction(1, 4)
+
+
+def test_trilinear_defect_sees_a_perturbed_a_entry():
+    """A[2][0] += 1: the change B[k,2] G[2,i] is largest at |B^T[2][k]| = 1/2,
+    |G[2][i]| = 1."""
+    pl = _f23()
+    pl.A[2][0] += 1
+    assert OP.trilinear_defect(pl) == Fraction(1, 2)
+
+
+def test_trilinear_defect_sees_a_perturbed_b_entry():
+    """B[3][3] += 1 (B^T[3][3] = 1 becomes 2): the (k, i, j) = (3, 2, 1) sum,
+    G[3][2] A[3][1] = 1 times the new entry, becomes 2 against a target of 1."""
+    pl = _f23()
+    pl.B[3][3] += 1
+    assert OP.trilinear_defect(pl) == 1
+
+
+def test_crt_idempotent_defect_sees_a_wrong_linear_factor():
+    """For the modulus a, M_0 = a^2 - 1 and N_0 = 1 / M_0(0) = -1.  Doubling
+    N_0 makes R_a[N_0 M_0] = 2 instead of 1: defect 1."""
+    pl = _f23()
+    assert pl.N[0] == (Fraction(-1),)
+    assert OP.crt_idempotent_defect(pl) == 0
+    pl.N[0] = (Fraction(-2),)
+    assert OP.crt_idempotent_defect(pl) == 1
+
+
+def test_crt_idempotent_defect_sees_a_wrong_quadratic_factor():
+    """For a^2 + 1 in {0, 1, -1, a^2+1, inf}: M_3 = a^3 - a = -2a mod a^2+1,
+    so N_3 = a/2 (since -2a * a/2 = -a^2 = 1).  With N_3 = a instead,
+    R[a (a^3 - a)] = -2a^2 = 2: defect 1."""
+    import copy
+    pl = copy.deepcopy(OP.build_plan("0,1,-1,a^2+1,inf", n_o=4))
+    assert pl.N[3] == (Fraction(0), Fraction(1, 2))
+    assert OP.crt_idempotent_defect(pl) == 0
+    pl.N[3] = (Fraction(0), Fraction(1))
+    assert OP.crt_idempotent_defect(pl) == 1
+
+
+@pytest.mark.parametrize("poly", ["a^3-1", "a^3-3a^2+3a-1", "a^3+2a^2+a+2", "a^3-1/2a^2+a-1/2", "a^3+a"])
+def test_reducible_cubics_rejected(poly):
+    """(a-1)(a^2+a+1), (a-1)^3, (a+2)(a^2+1), (a-1/2)(a^2+1) and a(a^2+1) have
+    a rational root, so they factor over Q (Section 2.1 asks for irreducible
+    moduli)."""
+    assert not OP.is_irreducible(P.monic(P.parse(poly)))
+    with pytest.raises(ValueError, match="reducible"):
+        OP.build_plan(f"0,-1,{poly},inf", n_o=4, inner="0,-1,1,-2,inf")
+
+
+@pytest.mark.parametrize("poly", ["a^3+2", "a^3-2", "a^3+a+1", "a^3-1/3a^2+1"])
+def test_irreducible_cubics_accepted(poly):
+    """No rational root: +-2 and +-1 are not roots of a^3 + 2, a^3 - 2 or
+    a^3 + a + 1 (values 10, 6, -6, ... 3, -1), nor is any +-p/q of 3a^3 - a^2 + 3."""
+    assert OP.is_irreducible(P.monic(P.parse(poly)))
+    pl = OP.build_plan(f"0,-1,{poly},inf", n_o=4, inner="0,-1,1,-2,inf")
+    assert OP.trilinear_defect(pl) == 0
