@@ -149,7 +149,11 @@ wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, 
 /* Release a plan (NULL is ignored).  Does not free a bound workspace. */
 void winograd_plan_destroy(wg_plan plan);
 
-/* alpha' = sum over finite moduli of (2 deg - 1), plus 1 for infinity. */
+/* alpha' = sum over finite moduli of (2 deg - 1), plus 1 for infinity: the
+ * number of Winograd-domain points per dimension, i.e. the rows of G and A
+ * that Algorithm 1 stacks (a degree-d modulus contributes the 2d - 1 rows of
+ * its inner Toom-Cook algorithm); alpha'^2 / m^2 is the ratio of Section 2.3,
+ * Table 1.  0 for a NULL plan. */
 int winograd_plan_alpha(wg_plan plan);
 
 /* The library carries input and output transform kernels with the
@@ -163,8 +167,10 @@ wg_status winograd_plan_builtin(wg_plan plan, int* id);
 /* m, r, alpha', input tile m + r - 1 and dtype of a plan. */
 wg_status winograd_plan_info(wg_plan plan, int* m, int* r, int* alpha, int* tile_in, int* dtype);
 
-/* Exact matrix 'G' (alpha' x r), 'A' (alpha' x m) or 'B' ((m+r-1) x alpha'),
- * row-major, into out[cap] (cap >= rows * cols). */
+/* Exact matrix 'G' (alpha' x r) or 'A' (alpha' x m) of Algorithm 1, or 'B'
+ * ((m+r-1) x alpha') of Algorithm 2 (B^W = [E C | vec(M)]), row-major, into
+ * out[cap] (cap >= rows * cols), each entry num/den in lowest terms with
+ * den > 0.  WG_ERR_ARG for another letter, a NULL pointer or a short cap. */
 wg_status winograd_plan_matrix(wg_plan plan, char which, wg_rational* out, size_t cap);
 
 /* The same matrix as the fp32 values the kernels use. */
@@ -210,8 +216,11 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
 /* U[xi][k][c] = (G g_kc G^T)[i][j]: eq. (2)'s kernel transform. */
 wg_status winograd_kernel_transform(wg_plan plan, const wg_tensor* w, void* U, hipStream_t stream);
 
-/* V[xi][t][c] = (B^T d_tc B)[i][j], d_tc the (m+2)^2 window of channel c whose
- * top-left input pixel is (ty*m - 1, tx*m - 1); pixels outside x read 0. */
+/* V[xi][t][c] = (B^T d_tc B)[i][j]: eq. (2)'s input transform, on the
+ * overlapping tiles of Section 2.3; d_tc is the (m+2)^2 window of channel c
+ * whose top-left input pixel is (ty*m - 1, tx*m - 1); pixels outside x read 0.
+ * x is [N][H][W][C] in the plan's dtype; V (caller-owned, 16-byte aligned)
+ * is written in the layout above, its pad channels C..Cp-1 as zeros. */
 wg_status winograd_input_transform(wg_plan plan, const wg_tensor* x, void* V, hipStream_t stream);
 
 /* Both transforms above in one launch (the first kernel of winograd_conv2d):
@@ -230,7 +239,9 @@ wg_status winograd_kernel_input_transform(wg_plan plan, const wg_tensor* w, cons
 wg_status winograd_contract(wg_plan plan, const void* V, const void* U, float* M, int64_t T,
                             int64_t C, int64_t K, hipStream_t stream);
 
-/* y[n][ty*m+o][tx*m+p][k] = (A^T M_tk A)[o][p], stored only inside H x W. */
+/* y[n][ty*m+o][tx*m+p][k] = (A^T M_tk A)[o][p]: eq. (2)'s output transform
+ * of the fp32 M above, rounded once to the plan's dtype and stored only
+ * inside H x W (y gives N, H, W and K).  M and y are caller-owned. */
 wg_status winograd_output_transform(wg_plan plan, const float* M, wg_tensor* y, hipStream_t stream);
 
 /* The fused path's kernel: y = output transform of the contraction of V and U

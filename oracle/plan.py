@@ -40,7 +40,7 @@ notes of the repository):
 * Moduli are made monic; they must be irreducible and pairwise coprime
   (Section 2.1).
 
-Option (an accuracy variant the paper names as complementary, Section 5):
+Option (an accuracy variant the paper's related work names as complementary, Section 4):
 ``factors="G"`` moves each CRT factor N_i from the input side to the kernel
 side.  Eq. (1) multiplies the residue product s_i = (g d) mod m_i by N_i; since
 (N_i g mod m_i)(d mod m_i) = N_i g d (mod m_i), the factor may multiply the

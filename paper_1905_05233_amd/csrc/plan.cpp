@@ -26,7 +26,7 @@
 // Option: the CRT factors N_i may instead multiply the kernel residues
 // ((N_i g mod m_i)(d mod m_i) = N_i g d mod m_i), giving G' = [vec(R_m[N_i
 // a^k])] and E_i = [vec(R_M[a^k M_i])]: the same exact algorithm with other
-// roundings (an accuracy variant of the kind Section 5 names as complementary).
+// roundings (an accuracy variant of the kind the related work of Section 4 names as complementary).
 #include "plan.hpp"
 
 #include <algorithm>

@@ -1,6 +1,6 @@
 """Polynomial-set search on the GPU.
 
-Section 4 of Barabasz & Gregg (arXiv 1905.05233) compares the floating-point
+Section 3.1 of Barabasz & Gregg (arXiv 1905.05233) compares the floating-point
 error of Winograd convolutions built from different modulus sets, on random
 data, against the ratio alpha'^2 / m^2 of multiplications per output; and it
 picks, for each CNN layer, the plan that suits it.  This module runs both on
@@ -9,7 +9,7 @@ the library's own kernels:
 * ``candidate_sets(m)`` enumerates modulus sets for F(m x m, 3 x 3): the first
   linear points of a fixed list of well-conditioned points (0, -1, 1, -1/2, 2,
   1/2, -2, ...), plus up to ``max_quadratic`` irreducible quadratics, plus the
-  pseudo-point infinity, with degrees summing to m + r - 1 (Section 3).
+  pseudo-point infinity, with degrees summing to m + r - 1 (Algorithms 1 and 2, Table 1).
 * ``sweep(...)`` convolves one seeded synthetic layer with every set and ranks
   them by relative L2 error.  The reference is the same layer, on the same
   dtype-rounded inputs, computed in fp32 by the F(2 x 2, 3 x 3) plan on points

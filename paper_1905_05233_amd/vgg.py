@@ -1,6 +1,6 @@
 """The VGG-16-shaped stack of thirteen 3x3 convolutions on the library.
 
-The paper's CNN experiments (Section 4) run VGG-16; here the stack has VGG-16's
+The paper's CNN experiments (Section 3.2, Tables 2 and 3) run VGG-16; here the stack has VGG-16's
 layer shapes with seeded random weights (N(0, 2/(9C)), seed 1 + layer) and a
 seeded half-normal input, and each layer uses the Winograd plan chosen for it
 from a candidate list (most accurate by default, see ``search.best_plan``).

@@ -1,4 +1,4 @@
-"""The polynomial-set search on the GPU (Section 4's error-versus-ratio sweep
+"""The polynomial-set search on the GPU (Section 3.1's error-versus-ratio sweep
 on seeded synthetic data).
 
 * The search's reference, the fp32 F(2x2,3x3) plan, is within 1e-6 of fp64
