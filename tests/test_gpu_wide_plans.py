@@ -1,17 +1,18 @@
 """The wider plan family on the GPU: larger output tiles with one degree-2
-modulus (alpha' = m + 3, the paper's Section 4 sweep), point sets without the
+modulus (alpha' = m + 3, the sweep of Section 3.2, Table 3), point sets without the
 pseudo-point infinity (Table 1's zero-linear columns), a degree-3 modulus, and
 layers whose channel counts span several 64-channel and 128-column blocks.
 
-Each case checks, on seeded half-normal data, that every output lies within
-the a-priori rounding bound of the exact convolution and that the rel-L2
-error against fp64 direct convolution is at most twice the oracle's
-same-algorithm, same-dtype error.
+Each case checks, on seeded half-normal data, that U and V equal the
+oracle's bit for bit, that every output lies within ``pair_bound`` of the
+oracle's (and, in fp32, within the a-priori rounding bound of the exact
+convolution), and that the rel-L2 error against fp64 direct convolution is at
+most twice the oracle's same-algorithm, same-dtype error.
 """
 import numpy as np
 import pytest
 
-from gpu_helpers import elementwise_bound, to_dev, to_np
+from gpu_helpers import check_layer, elementwise_bound, to_dev, to_np
 from oracle import conv as OC
 from oracle import fp as OF
 from oracle import plan as OP
@@ -46,11 +47,10 @@ def test_wide_plan_parity(spec, m, inner, dtype, shape):
     assert p.alpha == op.alpha
     y = to_np(p.conv2d(to_dev(x, dtype), to_dev(w, dtype))).astype(np.float64)
     y64 = OC.direct_f64(x, w)
-    yo = OC.winograd_emulated(x, w, op, dtype)
-    err_gpu, err_oracle = OC.rel_l2(y, y64), OC.rel_l2(yo, y64)
+    st = check_layer(p, op, x, w, dtype, y, label=f"wide {spec} {dtype} {shape}")
+    err_gpu, err_oracle = OC.rel_l2(y, y64), OC.rel_l2(st["y"], y64)
     print(f"[wide] alpha'={op.alpha} err_gpu={err_gpu:.3e} err_oracle={err_oracle:.3e}", flush=True)
     assert np.all(np.isfinite(y))
     assert err_gpu <= 2 * err_oracle
-    bound = elementwise_bound(x, w, op, dtype, y64)
-    assert np.all(np.abs(y - y64) <= bound)
-    assert np.all(np.abs(y - yo) <= 2 * bound)
+    if dtype == "f32":
+        assert np.all(np.abs(y - y64) <= elementwise_bound(x, w, op, dtype, y64))
