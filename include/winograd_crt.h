@@ -204,6 +204,27 @@ wg_status winograd_plan_set_workspace(wg_plan plan, void* dev_ptr, size_t bytes)
 wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
                           hipStream_t stream);
 
+/* Bytes of device workspace that winograd_conv2d_static has on each GPU. */
+#define WG_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* winograd_conv2d without a bound workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc).  The workspace (U, V and, on the
+ * separate path, M) is a 64 MiB array in the library's device memory, one
+ * copy per GPU, kept until the process ends; its address on a device is
+ * looked up on the first call with that device current.  The call itself
+ * allocates nothing: no hipMalloc, no hipFree.  Arguments, layouts, path
+ * choice and results are those of winograd_conv2d with the same plan (the
+ * plan's bound workspace is neither used nor needed).  A layer whose
+ * workspace (winograd_workspace_bytes) exceeds WG_STATIC_SCRATCH_BYTES is
+ * rejected with WG_ERR_WORKSPACE before anything is launched.  Every call on
+ * a GPU uses that GPU's one array: calls that overlap in time on one GPU
+ * (other streams, other threads) race and give wrong results; calls in
+ * order on one stream are safe.  Nothing in the array needs to start at zero
+ * (every kernel writes what a later one reads). */
+wg_status winograd_conv2d_static(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
+                                 hipStream_t stream);
+
 /* ---- Stage entry points (each launches one kernel of winograd_conv2d) ----
  * Intermediate layouts, with Cp = C rounded up to a multiple of 8,
  * Kp = K rounded up to a multiple of 8, T = N * ceil(H/m) * ceil(W/m) tiles,

@@ -81,6 +81,8 @@ def lib():
         "winograd_conv_path": (ctypes.c_int, [P, i64, i64, i64, i64, i64, ctypes.POINTER(ctypes.c_int)]),
         "winograd_conv2d": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),
                                            ctypes.POINTER(WgTensor), P]),
+        "winograd_conv2d_static": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),
+                                                  ctypes.POINTER(WgTensor), P]),
         "winograd_kernel_transform": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), P, P]),
         "winograd_input_transform": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), P, P]),
         "winograd_kernel_input_transform": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),

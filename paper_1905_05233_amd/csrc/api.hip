@@ -8,6 +8,7 @@
 
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -15,6 +16,12 @@
 #include "kernels.hpp"
 #include "plan.hpp"
 #include "winograd_crt.h"
+
+// Workspace of winograd_conv2d_static (U, V and M of one layer), one copy per
+// GPU, held until the process ends.  Host code never passes `scratch` itself
+// to a kernel (in host code the name is only a stand-in); it uses the device
+// address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[WG_STATIC_SCRATCH_BYTES];
 
 struct wg_plan_s {
     wg::Transforms tr;
@@ -175,6 +182,29 @@ Layout layout_for(const wg_plan_s* p, int64_t N, int64_t H, int64_t W, int64_t C
     L.m_off = L.v_off + (L.path == WG_PATH_FUSED_INPUT ? 0 : align256(vb));
     L.total = L.m_off + (L.path == WG_PATH_SEPARATE ? align256(mb) : 0);
     return L;
+}
+
+// Device address of `scratch` on the current device, looked up on the first
+// call made with that device current and kept per device.
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+wg_status static_scratch(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return from_hip(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxScratchDevices) return fail(WG_ERR_UNSUPPORTED, "device index beyond 63");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return from_hip(e, "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(WG_ERR_HIP, "hipGetSymbolAddress(scratch) returned a null address");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return WG_OK;
 }
 
 bool dims_ok(int64_t N, int64_t H, int64_t W, int64_t C, int64_t K) {
@@ -418,8 +448,14 @@ wg_status winograd_plan_set_workspace(wg_plan plan, void* dev_ptr, size_t bytes)
     return WG_OK;
 }
 
-wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
-                          hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The launches of winograd_conv2d with the workspace at ws (ws_bytes long,
+// 256-byte aligned; nullptr: none) after the argument checks.
+wg_status conv2d_with(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y, void* ws,
+                      size_t ws_bytes, bool static_ws, hipStream_t stream) {
     wg_status s = check_plan(plan);
     if (s != WG_OK) return s;
     if ((s = check_tensor(x, "x")) != WG_OK || (s = check_tensor(w, "w")) != WG_OK ||
@@ -432,10 +468,17 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
     if (!dims_ok(x->n, x->h, x->w, x->c, w->n)) return fail(WG_ERR_ARG, "layer sizes must be in [1, 2^31)");
     const Layout L = layout_for(plan, x->n, x->h, x->w, x->c, w->n);
     if (L.path < 0) return fail(WG_ERR_UNSUPPORTED, "the fused path does not support this layer shape");
-    if (!plan->ws) return fail(WG_ERR_WORKSPACE, "no workspace bound to the plan");
-    if (plan->ws_bytes < L.total)
-        return fail(WG_ERR_WORKSPACE, "workspace too small: need " + std::to_string(L.total) + " bytes");
-    auto* base = static_cast<unsigned char*>(plan->ws);
+    if (static_ws) {
+        if (L.total > ws_bytes)
+            return fail(WG_ERR_WORKSPACE, "layer needs " + std::to_string(L.total) +
+                                              " bytes of workspace, more than the " + std::to_string(ws_bytes) +
+                                              " bytes of the allocation-free entry point");
+    } else {
+        if (!ws) return fail(WG_ERR_WORKSPACE, "no workspace bound to the plan");
+        if (ws_bytes < L.total)
+            return fail(WG_ERR_WORKSPACE, "workspace too small: need " + std::to_string(L.total) + " bytes");
+    }
+    auto* base = static_cast<unsigned char*>(ws);
     void* U = base + L.u_off;
     void* V = base + L.v_off;
     auto* M = reinterpret_cast<float*>(base + L.m_off);
@@ -453,6 +496,25 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
         return from_hip(launch_co(dt, L.g, plan->otab, V, U, y->data, stream), "fused contraction");
     if ((s = from_hip(launch_ct(dt, L.g, V, U, M, stream), "contraction")) != WG_OK) return s;
     return from_hip(launch_ot(dt, L.g, plan->otab, M, y->data, plan->builtin, stream), "output transform");
+}
+
+}  // namespace
+
+extern "C" {
+
+wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
+                          hipStream_t stream) {
+    if (!plan) return fail(WG_ERR_ARG, "null plan");
+    return conv2d_with(plan, x, w, y, plan->ws, plan->ws_bytes, false, stream);
+}
+
+wg_status winograd_conv2d_static(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
+                                 hipStream_t stream) {
+    if (!plan) return fail(WG_ERR_ARG, "null plan");
+    void* ws = nullptr;
+    const wg_status s = static_scratch(&ws);
+    if (s != WG_OK) return s;
+    return conv2d_with(plan, x, w, y, ws, WG_STATIC_SCRATCH_BYTES, true, stream);
 }
 
 wg_status winograd_kernel_transform(wg_plan plan, const wg_tensor* w, void* U, hipStream_t stream) {

@@ -174,6 +174,18 @@ class Plan:
                                           _stream_handle(stream)))
         return y
 
+    def conv2d_static(self, x, w, y, stream=None):
+        """y = conv3x3(x, w) through winograd_conv2d_static: the library's own
+        per-GPU device workspace, nothing allocated (y must be given).  Calls
+        that overlap in time on one GPU race."""
+        self._check_dtype(x, "x")
+        self._check_dtype(w, "w")
+        self._check_dtype(y, "y")
+        xt, wt, yt = _tensor(x, "x"), _tensor(w, "w"), _tensor(y, "y")
+        N.check(self._lib.winograd_conv2d_static(self._h, ctypes.byref(xt), ctypes.byref(wt), ctypes.byref(yt),
+                                                 _stream_handle(stream)))
+        return y
+
     def bind_call(self, x, w, y, stream=None):
         """Marshal the arguments of one conv2d call once and return a
         zero-argument callable that launches it (for tight loops and graph
