@@ -307,3 +307,105 @@ def rel_l2(y, y_ref):
     den = np.sqrt(np.sum(y_ref * y_ref))
     num = np.sqrt(np.sum((y - y_ref) ** 2))
     return float(num / den) if den > 0 else float(num)
+
+
+# ---------------------------------------------------------------------------
+# 1D convolution F(m, 3) (Section 2.1's polynomial product on one row;
+# Section 3.1 studies its error beside the 2D form).  Layouts: x [N][L][C],
+# w [K][3][C], y [N][L][K]; y[n, l, k] = sum_{j, c} w[k, j, c] x[n, l+j-1, c]
+# with zero padding 1.  Output tiles of m values, input windows of m + 2
+# values starting at tx*m - 1.
+# ---------------------------------------------------------------------------
+
+def _check_shapes_1d(x_shape, w_shape):
+    if len(x_shape) != 3 or len(w_shape) != 3 or w_shape[1] != 3 or w_shape[2] != x_shape[2]:
+        raise ValueError("x must be [N][L][C], w must be [K][3][C] with the input's C")
+
+
+def direct1d_exact(x, w):
+    """The 1D layer by its definition in exact rationals; nested lists."""
+    N, L, C = len(x), len(x[0]), len(x[0][0])
+    K = len(w)
+    y = [[[Fraction(0)] * K for _ in range(L)] for _ in range(N)]
+    for n in range(N):
+        for l in range(L):
+            for k in range(K):
+                acc = Fraction(0)
+                for j in range(3):
+                    ll = l + j - 1
+                    if 0 <= ll < L:
+                        for c in range(C):
+                            acc += Fraction(w[k][j][c]) * Fraction(x[n][ll][c])
+                y[n][l][k] = acc
+    return y
+
+
+def direct1d_f64(x, w):
+    """The 1D layer in float64: 3 shifted [N*L x C] @ [C x K] products."""
+    x = np.asarray(x, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    _check_shapes_1d(x.shape, w.shape)
+    N, L, C = x.shape
+    xp = np.zeros((N, L + 2, C))
+    xp[:, 1:L + 1, :] = x
+    y = np.zeros((N, L, w.shape[0]))
+    for j in range(3):
+        y += xp[:, j:j + L, :] @ w[:, j, :].T
+    return y
+
+
+def winograd1d_exact(x, w, plan):
+    """A^T [(G g) (.) (B^T d)] on every tile and channel pair, exact."""
+    m, t, al = plan.n_o, plan.tile_in, plan.alpha
+    G, A, B = plan.G, plan.A, plan.B
+    N, L, C = len(x), len(x[0]), len(x[0][0])
+    K = len(w)
+    tl = -(-L // m)
+    U = [[[sum((G[a][i] * Fraction(w[k][i][c]) for i in range(3)), Fraction(0)) for a in range(al)]
+          for c in range(C)] for k in range(K)]
+    y = [[[Fraction(0)] * K for _ in range(L)] for _ in range(N)]
+    for n in range(N):
+        for tx in range(tl):
+            Vs = []
+            for c in range(C):
+                d = [Fraction(x[n][tx * m - 1 + u][c]) if 0 <= tx * m - 1 + u < L else Fraction(0) for u in range(t)]
+                Vs.append([sum((B[u][a] * d[u] for u in range(t)), Fraction(0)) for a in range(al)])
+            for k in range(K):
+                Mx = [sum((U[k][c][a] * Vs[c][a] for c in range(C)), Fraction(0)) for a in range(al)]
+                for o in range(m):
+                    if tx * m + o < L:
+                        y[n][tx * m + o][k] = sum((A[a][o] * Mx[a] for a in range(al)), Fraction(0))
+    return y
+
+
+def winograd1d_emulated_stages(x, w, plan, dtype):
+    """The 1D layer with the library's rounding points: U = G g and V = B^T d
+    as one fp32 pass each (ascending index, fused multiply-adds), rounded to
+    the dtype; M the fp32 channel sum; y = A^T M in one fp32 pass, rounded to
+    the dtype.  Returns U [al][K][C], V [al][N][tl][C], M [al][N][tl][K] and
+    y [N][L][K]."""
+    x = np.asarray(x, dtype=np.float32)
+    w = np.asarray(w, dtype=np.float32)
+    _check_shapes_1d(x.shape, w.shape)
+    G, A, B = plan_f32(plan)
+    m, t = plan.n_o, plan.tile_in
+    N, L, C = x.shape
+    tl = -(-L // m)
+    U = fp.to_dtype(_left(G, np.transpose(w, (1, 0, 2)), axis=0), dtype)           # [al][K][C]
+    xp = np.zeros((N, tl * m + 2, C), dtype=np.float32)
+    xp[:, 1:L + 1, :] = x
+    d = np.empty((t, N, tl, C), dtype=np.float32)
+    for u in range(t):
+        d[u] = xp[:, u:u + tl * m:m, :]
+    V = fp.to_dtype(_left(np.ascontiguousarray(B.T), d, axis=0), dtype)             # [al][N][tl][C]
+    al = V.shape[0]
+    M = np.empty((al, N, tl, w.shape[0]), dtype=np.float32)
+    for a in range(al):
+        M[a] = V[a] @ U[a].T
+    Y = fp.to_dtype(_left(np.ascontiguousarray(A.T), M, axis=0), dtype)             # [m][N][tl][K]
+    y = np.transpose(Y, (1, 2, 0, 3)).reshape(N, tl * m, -1)[:, :L, :]
+    return {"U": U, "V": V, "M": M, "y": np.ascontiguousarray(y)}
+
+
+def winograd1d_emulated(x, w, plan, dtype):
+    return winograd1d_emulated_stages(x, w, plan, dtype)["y"]
