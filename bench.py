@@ -1,23 +1,30 @@
 #!/usr/bin/env python3
 """Throughput of the Winograd convolution hot path on one MI355X (gfx950).
 
-One step = one full layer through eq. (2) of Barabasz & Gregg (arXiv
-1905.05233): kernel and input transforms (one launch), alpha'^2 batched
-matrix-core contraction and output transform (separate kernels, or one fused
-kernel where the library picks that path for the layer shape), on seeded
-synthetic inputs already resident in HBM.  Default workload: conv3x3 stride 1 pad 1, N=8, C=K=128, H=W=56, fp32,
-F(4x4,3x3) with points {0, 1, -1, 1/2, -1/2, inf}.
+Default workload: the VGG-16-shaped stack of thirteen conv3x3 stride-1 pad-1
+NHWC layers at N = 32 in bf16 (224^2 x 3 -> 64 up to 14^2 x 512 -> 512),
+seeded half-normal input and He-initialised random weights, each layer on the
+Winograd plan (Algorithms 1 and 2 of Barabasz & Gregg, arXiv 1905.05233)
+that is most accurate against float64 direct convolution on its own input.
+One step is one pass through the thirteen convolutions of eq. (2): kernel
+and input transforms (one launch), then the alpha'^2 batched matrix-core
+contraction and the output transform (separate kernels, or one fused kernel
+where the library picks that path), inputs already resident in HBM.  The
+ReLU and 2x2 max-pooling between layers (one HIP kernel each) run between the
+timed convolutions; the whole pass including them is reported too.
 
 Prints one JSON line: direct-equivalent TFLOP/s (2 N H W C K 9 flops per
-step), per-kernel average durations (HIP events on the launch stream), the
-roofline of the dominant kernel, the rel-L2 error against fp64 direct
-convolution, and the CPU oracle's throughput on the same workload.
+layer) from HIP events around each convolution (warm caches), the same with
+the caches flushed before every layer, per-layer and per-kernel durations,
+the roofline of the dominant (kernel, layer) launch, each layer's rel-L2
+error against float64 direct convolution, and the CPU oracle's throughput on
+a bounded sample of the same workload.
 
-    python bench.py [--steps K] [--warmup W] [--workload cfg2] [--plan 0]
+    python bench.py [--steps K] [--warmup W] [--dtype bf16|f16]
+    python bench.py --workload cfg2 [--plan 0]      # one configured layer
 
-``--workload cfg5`` runs the VGG-16-shaped stack instead (thirteen layers at
-N = 32, ``--dtype`` bf16 or f16, the most accurate candidate plan per layer);
-its step is one pass through the thirteen convolutions.
+``--profile-kernel NAME [--profile-layer L]`` launches only that stage kernel
+(of VGG layer L), ``--steps`` times, for rocprofv3 kernel traces and counters.
 """
 import argparse
 import ctypes
@@ -169,21 +176,93 @@ def roofline(dom, work, us, dtype):
     return roof
 
 
+def _vgg_layer_work(L, N, dtype):
+    from paper_1905_05233_amd import workloads as WL
+    wl = WL.Workload("vgg", N=N, H=L["hw"], W=L["hw"], C=L["C"], K=L["K"], dtype=dtype, plans=(),
+                     x_dist="halfnormal")
+    return algorithmic_work(wl, L["plan"].alpha, L["plan"].m)
+
+
+def _vgg_cpu_baseline(stack, trace, budget_s):
+    """The oracle on image 0 of the batch, layer by layer in order (each
+    layer on the GPU's own input for it), until ``budget_s`` is used: the
+    rounding-emulated Winograd of the layer's plan and, timed apart, the
+    float64 direct convolution.  Returns the cpu_baseline record."""
+    import numpy as np
+    from oracle import conv as OC
+    from oracle import plan as OP
+    t_emu = t_dir = 0.0
+    flops = 0
+    done = []
+    errs = {}
+    for i, (L, (xi, _)) in enumerate(zip(stack.layers, trace)):
+        if t_emu + t_dir >= budget_s:
+            break
+        x = xi[:1].float().cpu().numpy()
+        w = L["w"].float().cpu().numpy()
+        op = OP.build_plan(L["spec"].moduli, n_o=L["spec"].m, inner=L["spec"].inner)
+        t0 = time.perf_counter()
+        yo = OC.winograd_emulated(x, w, op, stack.dtype)
+        t1 = time.perf_counter()
+        y64 = OC.direct_f64(x, w)
+        t2 = time.perf_counter()
+        t_emu += t1 - t0
+        t_dir += t2 - t1
+        flops += 2 * L["hw"] * L["hw"] * L["C"] * L["K"] * 9
+        done.append(i)
+        errs[i] = OC.rel_l2(yo, y64)
+    threads = blas_threads()
+    return {
+        "value": round(flops / t_emu / 1e12, 6), "unit": "TFLOP/s (direct-equivalent)", "cores": threads,
+        "kind": "oracle",
+        "sample": f"image 0 of the batch through layers {done[0]}..{done[-1]} in order (each on the GPU's input "
+                  f"for it): the oracle's rounding-emulated Winograd of the layer's plan, {t_emu:.1f} s "
+                  f"(numpy; BLAS threads for the channel sums, one thread elsewhere)",
+        "cpu_count": os.cpu_count(), "blas_threads": threads,
+        "fp64_direct": {"value": round(flops / t_dir / 1e12, 6), "unit": "TFLOP/s", "seconds": round(t_dir, 2),
+                        "what": "the oracle's float64 direct convolution (9 shifted BLAS products) of the same "
+                                "sample"},
+        "oracle_rel_l2": {str(k): v for k, v in errs.items()},
+    }
+
+
 def run_vgg(a):
-    """cfg5: the VGG-16-shaped stack, N = 32, the most accurate candidate plan
-    per layer; a step is one pass through the thirteen convolutions (the ReLU
-    and pooling between them are not timed)."""
+    """The VGG-16-shaped stack, N = 32: a step is one pass through the
+    thirteen convolutions (the ReLU and pooling between them run in their own
+    kernel, outside the per-convolution events)."""
     import numpy as np
     import torch
 
-    from paper_1905_05233_amd import workloads as WL
-    from paper_1905_05233_amd.vgg import VggStack, relu_pool
+    from paper_1905_05233_amd import _native as NAT
+    from paper_1905_05233_amd import layer_ops
+    from paper_1905_05233_amd.vgg import VggStack
 
     dtype = a.dtype or "bf16"
     N = 32
     stack = VggStack(dtype)
     x = stack.input(N)
     stream = torch.cuda.current_stream()
+    _, trace = stack.forward(x, keep=True)
+    torch.cuda.synchronize()
+
+    if a.profile_kernel:
+        li = a.profile_layer
+        L = stack.layers[li]
+        xi = trace[li][0]
+        y = torch.empty((N, L["hw"], L["hw"], L["K"]), dtype=stack.tdt, device=x.device)
+        stages = make_stages(L["plan"], xi, L["w"], y, N, L["hw"], L["hw"], L["C"], L["K"], stream)
+        if a.profile_kernel not in stages:
+            print(f"bench.py: {a.profile_kernel} is not on layer {li}'s path ({list(stages)})", file=sys.stderr)
+            return 2
+        for fn in stages.values():
+            NAT.check(fn())
+        torch.cuda.synchronize()
+        for _ in range(a.steps):
+            NAT.check(stages[a.profile_kernel]())
+        torch.cuda.synchronize()
+        print(json.dumps({"profiled": a.profile_kernel, "layer": li, "launches": a.steps}))
+        return 0
+
     for _ in range(a.warmup):
         stack.forward(x)
     torch.cuda.synchronize()
@@ -195,67 +274,87 @@ def run_vgg(a):
     ms_per_step = float(per_layer.sum())
     flops = stack.direct_flops(N)
     value = flops / (ms_per_step * 1e-3) / 1e12
+    ms_pass = stack.timed_pass(x, a.steps)
+    # cold caches: a 512 MiB buffer overwritten before every convolution
+    flush = torch.empty(128 * 1024 * 1024, dtype=torch.float32, device=x.device)
+    cold = np.zeros(len(stack.layers))
+    for _ in range(a.steps):
+        _, ms = stack.timed_forward(x, flush=flush)
+        cold += np.array(ms)
+    cold /= a.steps
+    del flush
 
-    # per-kernel totals over the layers, each layer's stages timed back to back
-    reps = max(5, a.steps // 5)
+    # per-kernel durations, each layer's stages launched back to back
+    reps = max(5, a.steps)
+    layers, launches = [], []
     tot_us = {k: 0.0 for k in KERNEL_NAMES}
     tot_work = {k: {"bytes": 0, "flops": 0} for k in KERNEL_NAMES}
-    xi = x
-    layers = []
-    for i, L in enumerate(stack.layers):
+    for i, (L, (xi, yi)) in enumerate(zip(stack.layers, trace)):
         hw, C, K = L["hw"], L["C"], L["K"]
-        y = torch.empty((N, hw, hw, K), dtype=stack.tdt, device=x.device)
+        y = torch.empty_like(yi)
         stages = make_stages(L["plan"], xi, L["w"], y, N, hw, hw, C, K, stream)
         kus = time_kernels(stages, reps, stream)
-        wl = WL.Workload(f"vgg{i}", N=N, H=hw, W=hw, C=C, K=K, dtype=dtype, plans=(), x_dist="halfnormal")
-        work = algorithmic_work(wl, L["plan"].alpha, L["plan"].m)
-        for k in kus:
-            tot_us[k] += kus[k]
+        work = _vgg_layer_work(L, N, dtype)
+        for k, us in kus.items():
+            tot_us[k] += us
             tot_work[k]["bytes"] += work[k]["bytes"]
             tot_work[k]["flops"] += work[k].get("flops", 0)
+            launches.append((us, k, i, work[k]))
+        # accuracy of image 0 against the library's float64 direct convolution
+        ref = layer_ops.direct_conv_f64(xi[:1], L["w"])
+        err = layer_ops.rel_l2(yi[:1].contiguous(), ref)
         layers.append({"layer": i, "H": hw, "C": C, "K": K, "moduli": L["spec"].moduli, "m": L["spec"].m,
                        "alpha": L["plan"].alpha, "path": L["plan"].conv_path(N, hw, hw, C, K),
-                       "conv_ms": round(float(per_layer[i]), 4),
-                       "kernels_us": {k: round(v, 2) for k, v in kus.items()}})
-        xi = relu_pool(y, L["pool"])
-    dom = max(KERNEL_NAMES, key=lambda k: tot_us[k])
-    roof = roofline(dom, tot_work[dom], tot_us[dom], dtype)
-    roof["traffic"] = None
+                       "conv_ms": round(float(per_layer[i]), 4), "conv_ms_cold": round(float(cold[i]), 4),
+                       "kernels_us": {k: round(v, 2) for k, v in kus.items()},
+                       "rel_l2_image0": err})
+    us, dom, dl, dwork = max(launches, key=lambda r: r[0])
+    roof = roofline(dom, dwork, us, dtype)
+    roof["layer"] = dl
+    roof["traffic"] = load_traffic(dom, f"vgg16_{dtype}_l{dl}")
     used = [k for k in KERNEL_NAMES if tot_us[k] > 0]
     kernels = {k: {"total_us": round(tot_us[k], 2), "algorithmic_bytes": tot_work[k]["bytes"],
                    "GB_s": round(tot_work[k]["bytes"] / (tot_us[k] * 1e-6) / 1e9, 1)} for k in used}
     for k in ("contract", "contract_output", "input_contract_output"):
         if k in kernels:
             kernels[k]["TFLOP_s"] = round(tot_work[k]["flops"] / (tot_us[k] * 1e-6) / 1e12, 2)
+    errs = [r["rel_l2_image0"] for r in layers]
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s (direct-equivalent)",
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
-        "config": {"workload": f"VGG-16-shaped stack of 13 conv3x3 s1 p1 NHWC layers, N={N}, {dtype}, "
-                               f"most accurate candidate plan per layer (ReLU and 2x2 max-pool between "
-                               f"stages, not timed)", "N": N, "layers": layers},
+        "config": {"workload": f"VGG-16-shaped stack of 13 conv3x3 s1 p1 NHWC layers (224x224x3->64 .. "
+                               f"14x14x512->512), N={N}, {dtype}, the most accurate candidate plan per layer; "
+                               f"stands in for the paper's ImageNet/VGG16 runs", "N": N, "layers": layers},
+        "cold": {"ms_per_step": round(float(cold.sum()), 5),
+                 "value": round(flops / (float(cold.sum()) * 1e-3) / 1e12, 2),
+                 "how": "a 512 MiB device buffer overwritten before every convolution, outside its events"},
+        "pass_with_relu_pool": {"ms": round(ms_pass, 5),
+                                "value": round(flops / (ms_pass * 1e-3) / 1e12, 2),
+                                "how": "HIP events around whole back-to-back passes: 13 convolutions and the "
+                                       "ReLU/max-pool kernels"},
+        "rel_l2": {"max_over_layers_image0": max(errs), "cap": 5e-2, "pass": bool(max(errs) <= 5e-2),
+                   "reference": "the library's float64 direct convolution of the same layer input"},
         "kernels": kernels, "roofline": roof,
     }
     if a.cpu_seconds > 0:
-        from oracle import conv as OC
-        from oracle import plan as OP
-        t0 = time.perf_counter()
-        done = 0
-        xs = x[:1]
-        for L in stack.layers:
-            xa = xs.float().cpu().numpy()
-            op = OP.build_plan(L["spec"].moduli, n_o=L["spec"].m, inner=L["spec"].inner)
-            OC.winograd_emulated(xa, L["w"].float().cpu().numpy(), op, dtype)
-            done += 2 * L["hw"] * L["hw"] * L["C"] * L["K"] * 9
-            xs = relu_pool(L["plan"].conv2d(xs, L["w"]), L["pool"])
-            if time.perf_counter() - t0 >= a.cpu_seconds:
-                break
-        dt = time.perf_counter() - t0
-        out["cpu_baseline"] = {"value": round(done / dt / 1e12, 6), "unit": "TFLOP/s (direct-equivalent)",
-                               "cores": blas_threads(), "kind": "oracle",
-                               "sample": f"image 0 through the stack's layers in order, as far as {a.cpu_seconds:g} s "
-                                         f"allows, with the oracle's rounding-emulated Winograd ({dt:.1f} s)"}
+        out["cpu_baseline"] = _vgg_cpu_baseline(stack, trace, a.cpu_seconds)
     print(json.dumps(out), flush=True)
+    return 0
+
+
+def profile_copy(a, dev):
+    """A plain 256 MiB device copy, --steps times: the calibration of the
+    byte counters (its true traffic is known)."""
+    import torch
+    src = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(a.steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"profiled": "copy", "bytes_read_per_launch": src.numel() * 4,
+                      "bytes_written_per_launch": dst.numel() * 4, "launches": a.steps}))
     return 0
 
 
@@ -271,18 +370,20 @@ def blas_threads():
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="cfg2")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="vgg16", choices=("vgg16", "cfg5", "cfg1", "cfg2", "cfg3", "cfg4"),
+                    help="vgg16 (= cfg5, the default): the VGG-16-shaped stack; cfg1..cfg4: one layer")
     ap.add_argument("--plan", type=int, default=0)
     ap.add_argument("--dtype", default=None, choices=("f16", "bf16"),
-                    help="storage dtype of the cfg5 VGG-16 stack (default bf16)")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="storage dtype of the VGG-16 stack (default bf16)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="CPU oracle time budget (0 disables the cpu_baseline leg)")
     ap.add_argument("--graph", action="store_true", help="replay each step from a captured HIP graph")
     ap.add_argument("--profile-kernel", default=None, choices=KERNEL_NAMES + ("copy",),
                     help="only launch this kernel, --steps times (for counter collection); 'copy' "
                          "launches a plain 256 MiB device copy to calibrate the byte counters")
+    ap.add_argument("--profile-layer", type=int, default=1, help="VGG layer of --profile-kernel (0..12)")
     a = ap.parse_args(argv)
 
     if a.gpus != 1:
@@ -301,7 +402,9 @@ def main(argv=None):
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     dev = torch.device("cuda:0")
-    if a.workload == "cfg5":
+    if a.workload in ("vgg16", "cfg5"):
+        if a.profile_kernel == "copy":
+            return profile_copy(a, dev)
         return run_vgg(a)
     wl = WL.CONFIGS[a.workload]
     ps = wl.plans[a.plan]
@@ -318,15 +421,7 @@ def main(argv=None):
     stages = make_stages(plan, xd, wd, y, wl.N, wl.H, wl.W, wl.C, wl.K, stream)
 
     if a.profile_kernel == "copy":
-        src = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        for _ in range(a.steps):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"profiled": "copy", "bytes_read_per_launch": src.numel() * 4,
-                          "bytes_written_per_launch": dst.numel() * 4, "launches": a.steps}))
-        return 0
+        return profile_copy(a, dev)
     if a.profile_kernel:
         if a.profile_kernel not in stages:
             print(f"bench.py: {a.profile_kernel} is not on this layer's path ({list(stages)})", file=sys.stderr)
@@ -413,7 +508,9 @@ def main(argv=None):
             if time.perf_counter() - t0 >= a.cpu_seconds:
                 break
         dt = time.perf_counter() - t0
+        t1 = time.perf_counter()
         y64 = OC.direct_f64(x, w)
+        dt64 = time.perf_counter() - t1
         err_gpu = OC.rel_l2(y_gpu, y64)
         err_or = OC.rel_l2(yo, y64)
         out["rel_l2"] = {"gpu_vs_fp64_direct": err_gpu, "oracle_vs_fp64_direct": err_or, "cap": wl.cap,
@@ -422,7 +519,10 @@ def main(argv=None):
                                "unit": "TFLOP/s (direct-equivalent)", "cores": blas_threads(), "kind": "oracle",
                                "sample": f"{reps} full layer(s) of the same workload through the oracle's "
                                          f"rounding-emulated Winograd (numpy; BLAS threads for the channel "
-                                         f"sums, one thread elsewhere), {dt:.1f} s"}
+                                         f"sums, one thread elsewhere), {dt:.1f} s",
+                               "cpu_count": os.cpu_count(), "blas_threads": blas_threads(),
+                               "fp64_direct": {"value": round(wl.direct_flops / dt64 / 1e12, 6), "unit": "TFLOP/s",
+                                               "seconds": round(dt64, 2)}}
     print(json.dumps(out), flush=True)
     return 0
 

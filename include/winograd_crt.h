@@ -225,6 +225,20 @@ wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
 wg_status winograd_conv2d_static(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
                                  hipStream_t stream);
 
+/* ---- 1D convolution F(m, 3) ------------------------------------------------
+ * The same plan applied in one dimension (Section 2.1's polynomial product,
+ * y = A^T [(G g) (.) (B^T d)] on tiles of m outputs; Section 3.1 measures its
+ * error beside the 2D form): y[n][0][l][k] = sum_{j<3,c} w[k][0][j][c]
+ * x[n][0][l+j-1][c], zero padding 1, cross-correlation.  Tensors use the 4-D
+ * descriptor with height 1: x [N][1][L][C], w [K][1][3][C], y [N][1][L][K],
+ * storage dtype of the plan.  Rounding points as in 2D: fp32 transforms (one
+ * pass each), U and V rounded to the dtype, fp32 channel sums, y rounded once.
+ * The workspace (winograd_workspace_bytes_1d: U [alpha'][K][Cp],
+ * V [alpha'][T][Cp], M [alpha'][T][Kp] fp32, T = N ceil(L/m)) is the plan's
+ * bound one.  Asynchronous on stream; errors as winograd_conv2d. */
+wg_status winograd_workspace_bytes_1d(wg_plan plan, int64_t N, int64_t L, int64_t C, int64_t K, size_t* bytes);
+wg_status winograd_conv1d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y, hipStream_t stream);
+
 /* ---- Stage entry points (each launches one kernel of winograd_conv2d) ----
  * Intermediate layouts, with Cp = C rounded up to a multiple of 8,
  * Kp = K rounded up to a multiple of 8, T = N * ceil(H/m) * ceil(W/m) tiles,
@@ -279,6 +293,38 @@ wg_status winograd_contract_output(wg_plan plan, const void* V, const void* U, i
  * path is not available. */
 wg_status winograd_input_contract_output(wg_plan plan, const wg_tensor* x, const void* U, wg_tensor* y,
                                          hipStream_t stream);
+
+/* ---- Around the layer (not part of eq. (2)) ------------------------------ */
+
+/* y = ReLU(x) (pool == 0, y shaped like x) or y = 2x2 stride-2 max-pooling
+ * of ReLU(x) (pool == 1, y [N][H/2][W/2][C], odd last rows and columns
+ * dropped): the operations between the convolutions of the VGG-16 network of
+ * Section 3.2.  x and y are NHWC in dtype, 16-byte aligned, and must not
+ * overlap (an empty pooled y, from H or W equal to 1, may have a null data
+ * pointer: nothing is launched); ReLU maps NaN and -0 to +0.  Asynchronous
+ * on stream. */
+wg_status winograd_relu_pool(wg_dtype dtype, const wg_tensor* x, wg_tensor* y, int pool, hipStream_t stream);
+
+/* Direct convolution in float64, the reference of the error studies of
+ * Section 3.1: y[n][h][v][k] = sum w[k][i][j][c] x[n][h+i-1][v+j-1][c] over the
+ * 3x3 taps (w->h == 3, zero padding 1), or, with w->h == 1, the 1D
+ * convolution y[n][h][v][k] = sum_j,c w[k][0][j][c] x[n][h][v+j-1][c] of each
+ * row (zero padding 1 along W).  x [N][H][W][C] and w [K][w->h][3][C] are in
+ * dtype (each value is widened exactly); y [N][H][W][K] is float64, 8-byte
+ * aligned, caller-owned.  Asynchronous on stream. */
+wg_status winograd_direct_conv_f64(wg_dtype dtype, const wg_tensor* x, const wg_tensor* w, double* y,
+                                   hipStream_t stream);
+
+/* Doubles of the sums buffer of winograd_sq_error_sums. */
+#define WG_SQ_SUMS_DOUBLES 514
+
+/* sums[0] = sum_i (y[i] - ref[i])^2 and sums[1] = sum_i ref[i]^2 over n
+ * values, in float64, in a fixed order (the same bits on every run), so that
+ * sqrt(sums[0] / sums[1]) is the relative L2 error of y (dtype) against the
+ * float64 reference.  sums (device, WG_SQ_SUMS_DOUBLES doubles, 8-byte
+ * aligned) also holds the per-block partial sums.  Asynchronous on stream. */
+wg_status winograd_sq_error_sums(wg_dtype dtype, const void* y, const double* ref, int64_t n, double* sums,
+                                 hipStream_t stream);
 
 /* Message describing the last error of the calling thread ("" if none). */
 const char* winograd_last_error(void);

@@ -11,6 +11,7 @@ STATUS_NAMES = {
     5: "WG_ERR_UNSUPPORTED", 6: "WG_ERR_OVERFLOW", 7: "WG_ERR_WORKSPACE", 8: "WG_ERR_HIP", 9: "WG_ERR_INTERNAL",
 }
 DTYPE_CODES = {"f32": 0, "f16": 1, "bf16": 2}
+SQ_SUMS_DOUBLES = 514   # WG_SQ_SUMS_DOUBLES
 
 
 class WgRational(ctypes.Structure):
@@ -81,6 +82,9 @@ def lib():
         "winograd_conv_path": (ctypes.c_int, [P, i64, i64, i64, i64, i64, ctypes.POINTER(ctypes.c_int)]),
         "winograd_conv2d": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),
                                            ctypes.POINTER(WgTensor), P]),
+        "winograd_workspace_bytes_1d": (ctypes.c_int, [P, i64, i64, i64, i64, ctypes.POINTER(sz)]),
+        "winograd_conv1d": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),
+                                           ctypes.POINTER(WgTensor), P]),
         "winograd_conv2d_static": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),
                                                   ctypes.POINTER(WgTensor), P]),
         "winograd_kernel_transform": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), P, P]),
@@ -92,6 +96,11 @@ def lib():
         "winograd_contract_output": (ctypes.c_int, [P, P, P, i64, ctypes.POINTER(WgTensor), P]),
         "winograd_input_contract_output": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), P, ctypes.POINTER(WgTensor),
                                                           P]),
+        "winograd_relu_pool": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),
+                                              ctypes.c_int, P]),
+        "winograd_direct_conv_f64": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(WgTensor),
+                                                    ctypes.POINTER(WgTensor), P, P]),
+        "winograd_sq_error_sums": (ctypes.c_int, [ctypes.c_int, P, P, i64, P, P]),
         "winograd_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sigs.items():

@@ -38,6 +38,8 @@ UNITS = [
     ("fused.hip", DEVICE + ["-DWG_DTYPE=0"], "fused_f32.o"),
     ("fused.hip", DEVICE + ["-DWG_DTYPE=1"], "fused_f16.o"),
     ("fused.hip", DEVICE + ["-DWG_DTYPE=2"], "fused_bf16.o"),
+    ("layer_ops.hip", DEVICE, "layer_ops.o"),
+    ("conv1d.hip", DEVICE, "conv1d.o"),
 ]
 
 

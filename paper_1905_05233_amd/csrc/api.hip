@@ -498,9 +498,75 @@ wg_status conv2d_with(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_t
     return from_hip(launch_ot(dt, L.g, plan->otab, M, y->data, plan->builtin, stream), "output transform");
 }
 
+// Workspace of the 1D path: U [alpha'][K][Cp], V [alpha'][T][Cp], M [alpha'][T][Kp].
+struct Layout1d {
+    wg::Geometry g;
+    size_t u_off, v_off, m_off, total;
+};
+
+Layout1d layout_1d(const wg_plan_s* p, int64_t N, int64_t L, int64_t C, int64_t K) {
+    Layout1d o;
+    o.g = wg::make_geometry_1d(N, L, C, K, p->tr.m, p->tr.alpha);
+    const size_t es = static_cast<size_t>(wg::dtype_bytes(p->dtype));
+    const size_t al = static_cast<size_t>(p->tr.alpha);
+    o.u_off = 0;
+    o.v_off = align256(al * static_cast<size_t>(K) * static_cast<size_t>(o.g.Cp) * es);
+    o.m_off = o.v_off + align256(al * static_cast<size_t>(o.g.T) * static_cast<size_t>(o.g.Cp) * es);
+    o.total = o.m_off + align256(al * static_cast<size_t>(o.g.T) * static_cast<size_t>(o.g.Kp) * sizeof(float));
+    return o;
+}
+
 }  // namespace
 
 extern "C" {
+
+wg_status winograd_workspace_bytes_1d(wg_plan plan, int64_t N, int64_t L, int64_t C, int64_t K, size_t* bytes) {
+    if (!plan || !bytes) return fail(WG_ERR_ARG, "null argument");
+    if (!dims_ok(N, 1, L, C, K)) return fail(WG_ERR_ARG, "layer sizes must be in [1, 2^31)");
+    *bytes = layout_1d(plan, N, L, C, K).total;
+    return WG_OK;
+}
+
+wg_status winograd_conv1d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y, hipStream_t stream) {
+    if (!plan) return fail(WG_ERR_ARG, "null plan");
+    wg_status s;
+    if ((s = check_tensor(x, "x")) != WG_OK || (s = check_tensor(w, "w")) != WG_OK ||
+        (s = check_tensor(y, "y")) != WG_OK)
+        return s;
+    if (x->h != 1 || w->h != 1 || w->w != 3 || w->c != x->c)
+        return fail(WG_ERR_ARG, "x must be [N][1][L][C] and w [K][1][3][C] with the input's C");
+    if (y->n != x->n || y->h != 1 || y->w != x->w || y->c != w->n) return fail(WG_ERR_ARG, "y must be [N][1][L][K]");
+    if (!dims_ok(x->n, 1, x->w, x->c, w->n)) return fail(WG_ERR_ARG, "layer sizes must be in [1, 2^31)");
+    if (plan->tr.r != 3) return fail(WG_ERR_UNSUPPORTED, "only 3-tap kernels");
+    const Layout1d L = layout_1d(plan, x->n, x->w, x->c, w->n);
+    if (!plan->ws) return fail(WG_ERR_WORKSPACE, "no workspace bound to the plan");
+    if (plan->ws_bytes < L.total)
+        return fail(WG_ERR_WORKSPACE, "workspace too small: need " + std::to_string(L.total) + " bytes");
+    auto* base = static_cast<unsigned char*>(plan->ws);
+    void* U = base + L.u_off;
+    void* V = base + L.v_off;
+    auto* M = reinterpret_cast<float*>(base + L.m_off);
+    hipError_t e;
+    switch (plan->dtype) {
+        case 0: e = wg::launch_kernel_transform_1d_t<0>(L.g, plan->ktab, w->data, U, stream); break;
+        case 1: e = wg::launch_kernel_transform_1d_t<1>(L.g, plan->ktab, w->data, U, stream); break;
+        default: e = wg::launch_kernel_transform_1d_t<2>(L.g, plan->ktab, w->data, U, stream); break;
+    }
+    if ((s = from_hip(e, "1D kernel transform")) != WG_OK) return s;
+    switch (plan->dtype) {
+        case 0: e = wg::launch_input_transform_1d_t<0>(L.g, plan->itab, x->data, V, stream); break;
+        case 1: e = wg::launch_input_transform_1d_t<1>(L.g, plan->itab, x->data, V, stream); break;
+        default: e = wg::launch_input_transform_1d_t<2>(L.g, plan->itab, x->data, V, stream); break;
+    }
+    if ((s = from_hip(e, "1D input transform")) != WG_OK) return s;
+    if ((s = from_hip(launch_ct(plan->dtype, L.g, V, U, M, stream), "contraction")) != WG_OK) return s;
+    switch (plan->dtype) {
+        case 0: e = wg::launch_output_transform_1d_t<0>(L.g, plan->otab, M, y->data, stream); break;
+        case 1: e = wg::launch_output_transform_1d_t<1>(L.g, plan->otab, M, y->data, stream); break;
+        default: e = wg::launch_output_transform_1d_t<2>(L.g, plan->otab, M, y->data, stream); break;
+    }
+    return from_hip(e, "1D output transform");
+}
 
 wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
                           hipStream_t stream) {
@@ -601,6 +667,68 @@ wg_status winograd_input_contract_output(wg_plan plan, const wg_tensor* x, const
         return fail(WG_ERR_UNSUPPORTED, "the input transform is not fused for this layer shape");
     return from_hip(launch_ico(plan->dtype, g, plan->itab, plan->otab, x->data, U, y->data, stream),
                     "fused input transform and contraction");
+}
+
+wg_status winograd_relu_pool(wg_dtype dtype, const wg_tensor* x, wg_tensor* y, int pool, hipStream_t stream) {
+    wg_status s;
+    if ((s = check_tensor(x, "x")) != WG_OK) return s;
+    if (!y) return fail(WG_ERR_ARG, "null tensor y");
+    if (dtype != WG_F32 && dtype != WG_F16 && dtype != WG_BF16) return fail(WG_ERR_UNSUPPORTED, "unknown dtype");
+    if (pool != 0 && pool != 1) return fail(WG_ERR_ARG, "pool must be 0 or 1");
+    if (!dims_ok(x->n, x->h, x->w, x->c, 1)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
+    const int64_t ho = pool ? x->h / 2 : x->h, wo = pool ? x->w / 2 : x->w;
+    if (y->n != x->n || y->h != ho || y->w != wo || y->c != x->c)
+        return fail(WG_ERR_ARG, pool ? "y must be [N][H/2][W/2][C]" : "y must be shaped like x");
+    if (ho == 0 || wo == 0) return WG_OK;   // pooling a single row or column: nothing to store
+    if ((s = check_tensor(y, "y")) != WG_OK) return s;
+    const int64_t es = wg::dtype_bytes(dtype);
+    const auto* xb = static_cast<const unsigned char*>(x->data);
+    const auto* yb = static_cast<const unsigned char*>(y->data);
+    const int64_t xbytes = x->n * x->h * x->w * x->c * es, ybytes = y->n * y->h * y->w * y->c * es;
+    if (xb < yb + ybytes && yb < xb + xbytes) return fail(WG_ERR_ARG, "x and y overlap");
+    hipError_t e;
+    switch (dtype) {
+        case WG_F32: e = wg::launch_relu_pool_t<0>(x->data, y->data, x->n, x->h, x->w, x->c, pool, stream); break;
+        case WG_F16: e = wg::launch_relu_pool_t<1>(x->data, y->data, x->n, x->h, x->w, x->c, pool, stream); break;
+        default: e = wg::launch_relu_pool_t<2>(x->data, y->data, x->n, x->h, x->w, x->c, pool, stream); break;
+    }
+    return from_hip(e, "relu/max-pool");
+}
+
+wg_status winograd_direct_conv_f64(wg_dtype dtype, const wg_tensor* x, const wg_tensor* w, double* y,
+                                   hipStream_t stream) {
+    wg_status s;
+    if ((s = check_tensor(x, "x")) != WG_OK || (s = check_tensor(w, "w")) != WG_OK) return s;
+    if (!y || (reinterpret_cast<uintptr_t>(y) & 7u) != 0) return fail(WG_ERR_ARG, "y must be an 8-byte aligned device pointer");
+    if (dtype != WG_F32 && dtype != WG_F16 && dtype != WG_BF16) return fail(WG_ERR_UNSUPPORTED, "unknown dtype");
+    if ((w->h != 3 && w->h != 1) || w->w != 3 || w->c != x->c)
+        return fail(WG_ERR_ARG, "w must be [K][3][3][C] or [K][1][3][C] with the input's C");
+    if (!dims_ok(x->n, x->h, x->w, x->c, w->n)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
+    const int kh = static_cast<int>(w->h);
+    hipError_t e;
+    switch (dtype) {
+        case WG_F32: e = wg::launch_direct_f64_t<0>(x->data, w->data, y, x->n, x->h, x->w, x->c, w->n, kh, stream); break;
+        case WG_F16: e = wg::launch_direct_f64_t<1>(x->data, w->data, y, x->n, x->h, x->w, x->c, w->n, kh, stream); break;
+        default: e = wg::launch_direct_f64_t<2>(x->data, w->data, y, x->n, x->h, x->w, x->c, w->n, kh, stream); break;
+    }
+    return from_hip(e, "float64 direct convolution");
+}
+
+wg_status winograd_sq_error_sums(wg_dtype dtype, const void* y, const double* ref, int64_t n, double* sums,
+                                 hipStream_t stream) {
+    static_assert(WG_SQ_SUMS_DOUBLES == wg::kSqSumDoubles, "sums buffer size");
+    if (!y || !ref || !sums) return fail(WG_ERR_ARG, "null pointer");
+    if ((reinterpret_cast<uintptr_t>(ref) & 7u) != 0 || (reinterpret_cast<uintptr_t>(sums) & 7u) != 0)
+        return fail(WG_ERR_ARG, "ref and sums must be 8-byte aligned");
+    if (n < 0) return fail(WG_ERR_ARG, "n must be non-negative");
+    if (dtype != WG_F32 && dtype != WG_F16 && dtype != WG_BF16) return fail(WG_ERR_UNSUPPORTED, "unknown dtype");
+    hipError_t e;
+    switch (dtype) {
+        case WG_F32: e = wg::launch_sq_sums_t<0>(y, ref, n, sums, stream); break;
+        case WG_F16: e = wg::launch_sq_sums_t<1>(y, ref, n, sums, stream); break;
+        default: e = wg::launch_sq_sums_t<2>(y, ref, n, sums, stream); break;
+    }
+    return from_hip(e, "error sums");
 }
 
 const char* winograd_last_error(void) { return g_last_error.c_str(); }

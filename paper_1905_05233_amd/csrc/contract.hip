@@ -460,7 +460,7 @@ hipError_t launch_stream(const Geometry& g, const void* V, const void* U, float*
                          hipStream_t stream) {
     const int num_mb = static_cast<int>((g.T + kStreamRows - 1) / kStreamRows);
     const int num_nb = static_cast<int>((g.K + kStreamCols - 1) / kStreamCols);
-    const int64_t n_items = static_cast<int64_t>(num_mb) * num_nb * g.alpha * g.alpha;
+    const int64_t n_items = static_cast<int64_t>(num_mb) * num_nb * g.planes;
     const int64_t grid = std::min<int64_t>(n_items, device_cu_count());
     hipLaunchKernelGGL((contract_stream_kernel<D, NCH>), dim3(static_cast<unsigned>(grid)), dim3(stream_threads(NCH)), 0,
                        stream, static_cast<const unsigned char*>(V), static_cast<const unsigned char*>(U),
@@ -496,7 +496,7 @@ hipError_t launch_contract_t(const Geometry& g, const void* V, const void* U, fl
     if (fits32 && row_bytes <= 512) return launch_stream<D, 8>(g, V, U, M, row_bytes, stream);
     const int num_mb = static_cast<int>((g.T + kBM - 1) / kBM);
     const int num_nb = static_cast<int>((g.K + kBN - 1) / kBN);
-    const int64_t blocks = static_cast<int64_t>(num_mb) * num_nb * g.alpha * g.alpha;
+    const int64_t blocks = static_cast<int64_t>(num_mb) * num_nb * g.planes;
     // the block kernel addresses its 128 rows of V and of U with 32-bit offsets
     if (blocks > 0x7fffffff || std::max(kBM, kBN) * row_bytes >= 0xffff0000LL) return hipErrorInvalidValue;
     hipLaunchKernelGGL(contract_kernel<D>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream,

@@ -526,7 +526,7 @@ int pick_wt(const Geometry& g, int kw) {
 template <>
 bool contract_output_supported_t<WG_DTYPE>(const Geometry& g) {
     const int64_t rb = g.Cp * (WG_DTYPE == 0 ? 4 : 2);
-    if (g.t > 8 || !transform_shape_supported(g.t, g.alpha)) return false;
+    if (g.t > 8 || (g.t & 1) != 0 || !transform_shape_supported(g.t, g.alpha)) return false;
     // 32-bit buffer offsets: within a plane, and for every staged row of a block
     return g.T * rb < 0xffff0000LL && g.K * rb < 0xffff0000LL && rb <= (1 << 20);
 }

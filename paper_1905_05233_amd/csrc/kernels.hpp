@@ -25,6 +25,7 @@ struct Geometry {
     int m, t, alpha;
     int64_t th, tw, T;  // tiles along H, along W, total
     int64_t Cp, Kp;     // channel strides of U / V and of M
+    int64_t planes;     // Winograd-domain points: alpha'^2 (2D) or alpha' (1D)
 };
 
 inline int64_t round_up(int64_t v, int64_t q) { return (v + q - 1) / q * q; }
@@ -38,10 +39,21 @@ inline Geometry make_geometry(int64_t N, int64_t H, int64_t W, int64_t C, int64_
     g.T = N * g.th * g.tw;
     g.Cp = round_up(C, 8);
     g.Kp = round_up(K, 8);
+    g.planes = static_cast<int64_t>(alpha) * alpha;
     return g;
 }
 
-// (input tile m + 2, alpha') shapes with compiled input/output transforms:
+// A 1D layer (rows of length W = L, H = 1, a 1 x 3 kernel): tiles of m
+// outputs along W only, alpha' domain points.
+inline Geometry make_geometry_1d(int64_t N, int64_t L, int64_t C, int64_t K, int m, int alpha) {
+    Geometry g = make_geometry(N, 1, L, C, K, m, alpha);
+    g.th = 1;
+    g.T = N * g.tw;
+    g.planes = alpha;
+    return g;
+}
+
+// (input tile m + 2, alpha') shapes with compiled 2D input/output transforms:
 // even m from 2 to 12 and alpha' = m + 2 + q, where q = 0..3 counts the extra
 // multiplications per dimension that degree-2 moduli add (q = 0..4 for m = 6,
 // the all-quadratic F(6x6) column of Table 1), capped at alpha' = 16.
@@ -53,9 +65,15 @@ inline Geometry make_geometry(int64_t N, int64_t H, int64_t W, int64_t C, int64_
     X(12, 12) X(12, 13) X(12, 14) X(12, 15)                      \
     X(14, 14) X(14, 15) X(14, 16)
 
+// Odd output tiles m = 3, 5, 7 (input tiles 5, 7, 9) with all-linear sets or
+// one degree-2 modulus: the tile sizes of the random-data study of Section
+// 3.1.  Separate path only (the fused kernel takes even tiles).
+#define WG_TRANSFORM_SHAPES_ODD(X) X(5, 5) X(5, 6) X(7, 7) X(7, 8) X(9, 9) X(9, 10)
+
 inline bool transform_shape_supported(int t, int alpha) {
 #define WG_SHAPE_TEST(TT, A) if (t == TT && alpha == A) return true;
     WG_TRANSFORM_SHAPES(WG_SHAPE_TEST)
+    WG_TRANSFORM_SHAPES_ODD(WG_SHAPE_TEST)
 #undef WG_SHAPE_TEST
     return false;
 }
@@ -94,6 +112,36 @@ template <int D> bool input_contract_output_supported_t(const Geometry& g);
 template <int D>
 hipError_t launch_input_contract_output_t(const Geometry& g, const InputTable& itab, const OutputTable& otab,
                                           const void* x, const void* U, void* y, hipStream_t stream);
+
+// Around the layer (layer_ops.hip): ReLU, optionally followed by 2x2 stride-2
+// max-pooling (NHWC, storage dtype D); a float64 direct convolution with a
+// kernel of kh x 3 taps (kh = 3: pad 1 in both directions; kh = 1: a 1D
+// convolution along W, pad 1); the float64 sums of (y - ref)^2 and ref^2
+// over n values into sums[0], sums[1] (sums[2 ..] holds the kSqSumPartials
+// per-block partial pairs).
+constexpr int kSqSumDoubles = 2 + 2 * 256;
+template <int D>
+hipError_t launch_relu_pool_t(const void* x, void* y, int64_t N, int64_t H, int64_t W, int64_t C, bool pool,
+                              hipStream_t stream);
+template <int D>
+hipError_t launch_direct_f64_t(const void* x, const void* w, double* y, int64_t N, int64_t H, int64_t W, int64_t C,
+                               int64_t K, int kh, hipStream_t stream);
+template <int D>
+hipError_t launch_sq_sums_t(const void* y, const double* ref, int64_t n, double* sums, hipStream_t stream);
+
+// 1D F(m, 3) (conv1d.hip): kernel transform U [alpha'][K][Cp] from w
+// [K][1][3][C], input transform V [alpha'][T][Cp] from x [N][1][L][C], output
+// transform y [N][1][L][K] from M [alpha'][T][Kp] (the contraction is
+// launch_contract_t with g.planes = alpha').
+template <int D>
+hipError_t launch_kernel_transform_1d_t(const Geometry& g, const KernelTable& tab, const void* w, void* U,
+                                        hipStream_t stream);
+template <int D>
+hipError_t launch_input_transform_1d_t(const Geometry& g, const InputTable& tab, const void* x, void* V,
+                                       hipStream_t stream);
+template <int D>
+hipError_t launch_output_transform_1d_t(const Geometry& g, const OutputTable& tab, const float* M, void* y,
+                                        hipStream_t stream);
 
 // Compute units of the current device (cached per device).
 int device_cu_count();

@@ -582,6 +582,7 @@ hipError_t launch_input_transform_t(const Geometry& g, const InputTable& tab, co
 #define WG_IT_CASE(TT, A) \
     if (g.t == TT && g.alpha == A) return launch_it<Elem, TT, A, RuntimeCoefs>(g, tab, xp, vp, stream);
     WG_TRANSFORM_SHAPES(WG_IT_CASE)
+    WG_TRANSFORM_SHAPES_ODD(WG_IT_CASE)
 #undef WG_IT_CASE
     return hipErrorInvalidValue;
 }
@@ -614,6 +615,7 @@ hipError_t launch_kernel_input_transform_t(const Geometry& g, const KernelTable&
     if constexpr (TT <= 8)                                                                                 \
         if (g.t == TT && g.alpha == A) return launch_kit<Elem, TT, A, RuntimeCoefs>(g, ktab, itab, wp, xp, up, vp, stream);
     WG_TRANSFORM_SHAPES(WG_KIT_CASE)
+    WG_TRANSFORM_SHAPES_ODD(WG_KIT_CASE)
 #undef WG_KIT_CASE
     return hipErrorInvalidValue;
 }
@@ -636,6 +638,7 @@ hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, 
 #define WG_OT_CASE(TT, A) \
     if (g.t == TT && g.alpha == A) return launch_ot<Elem, TT, A, RuntimeCoefs>(g, tab, M, yp, stream);
     WG_TRANSFORM_SHAPES(WG_OT_CASE)
+    WG_TRANSFORM_SHAPES_ODD(WG_OT_CASE)
 #undef WG_OT_CASE
     return hipErrorInvalidValue;
 }

@@ -172,6 +172,47 @@ class Plan:
         xt, wt, yt = _tensor(x, "x"), _tensor(w, "w"), _tensor(y, "y")
         N.check(self._lib.winograd_conv2d(self._h, ctypes.byref(xt), ctypes.byref(wt), ctypes.byref(yt),
                                           _stream_handle(stream)))
+        self._keep_for(stream, y)
+        return y
+
+    def _keep_for(self, stream, y):
+        """Memory allocated here on the current stream but used on another
+        one: keep the caching allocator from reusing it before that stream's
+        work is done."""
+        if stream is not None and stream != torch.cuda.current_stream(y.device):
+            y.record_stream(stream)
+            if self._ws is not None:
+                self._ws.record_stream(stream)
+
+    def workspace_bytes_1d(self, N_, L, C, K):
+        out = ctypes.c_size_t()
+        N.check(self._lib.winograd_workspace_bytes_1d(self._h, N_, L, C, K, ctypes.byref(out)))
+        return out.value
+
+    def conv1d(self, x, w, y=None, workspace=None, stream=None):
+        """1D F(m, 3): y [N][L][K] = conv(x [N][L][C], w [K][3][C]), stride 1,
+        padding 1, along L (the descriptors carry height 1)."""
+        self._check_dtype(x, "x")
+        self._check_dtype(w, "w")
+        if x.dim() != 3 or w.dim() != 3 or w.shape[1] != 3 or w.shape[2] != x.shape[2]:
+            raise ValueError("x must be [N][L][C] and w [K][3][C]")
+        Nn, L, C = x.shape
+        K = w.shape[0]
+        if y is None:
+            y = torch.empty((Nn, L, K), dtype=x.dtype, device=x.device)
+        self._check_dtype(y, "y")
+        need = self.workspace_bytes_1d(Nn, L, C, K)
+        if workspace is None:
+            if self._ws is None or self._ws.numel() < need or self._ws.device != x.device:
+                self.bind_workspace(torch.empty(need, dtype=torch.uint8, device=x.device))
+        else:
+            self.bind_workspace(workspace)
+        xt = _tensor(x.unsqueeze(1), "x")
+        wt = _tensor(w.unsqueeze(1), "w")
+        yt = _tensor(y.unsqueeze(1), "y")
+        N.check(self._lib.winograd_conv1d(self._h, ctypes.byref(xt), ctypes.byref(wt), ctypes.byref(yt),
+                                          _stream_handle(stream)))
+        self._keep_for(stream, y)
         return y
 
     def conv2d_static(self, x, w, y, stream=None):

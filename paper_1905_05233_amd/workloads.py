@@ -10,7 +10,10 @@ chosen.  Each consumer rounds float32 to fp16/bf16 itself.
 Distributions (CNN-layer-shaped data):
   * ``uniform``:    x ~ U[-1, 1]
   * ``halfnormal``: x ~ |N(0, 1)|  (post-ReLU activations)
-  * weights always N(0, 2 / (9 C))  (He initialisation of a 3x3xC filter)
+  * ``normal_clip1``: x and the weights ~ N(0, 1) restricted to (-1, 1)
+    (values redrawn until they fall inside; the random data of the error
+    study of Section 3.1)
+  * weights otherwise N(0, 2 / (9 C))  (He initialisation of a 3x3xC filter)
 """
 from dataclasses import dataclass, field
 
@@ -57,6 +60,16 @@ class Workload:
         return 2 * self.N * self.H * self.W * self.C * self.K * 9
 
 
+def _normal_in_unit(rng, shape):
+    """N(0, 1) values restricted to (-1, 1) by redrawing those outside."""
+    v = rng.standard_normal(size=shape)
+    bad = np.abs(v) >= 1.0
+    while np.any(bad):
+        v[bad] = rng.standard_normal(size=int(np.sum(bad)))
+        bad = np.abs(v) >= 1.0
+    return v
+
+
 def draw_inputs(N, H, W, C, K, x_dist, seed, w_seed=None):
     """x [N][H][W][C] and w [K][3][3][C] as float32 arrays.
 
@@ -71,12 +84,16 @@ def draw_inputs(N, H, W, C, K, x_dist, seed, w_seed=None):
         x = rng.integers(-1, 2, size=(N, H, W, C)).astype(np.float64)
     elif x_dist == "int2":
         x = rng.integers(-2, 3, size=(N, H, W, C)).astype(np.float64)
+    elif x_dist == "normal_clip1":
+        x = _normal_in_unit(rng, (N, H, W, C))
     else:
         raise ValueError(f"unknown distribution {x_dist!r}")
     wrng = rng if w_seed is None else np.random.Generator(np.random.PCG64(w_seed))
     if x_dist in ("ternary", "int2"):
         lo, hi = (-1, 2) if x_dist == "ternary" else (-2, 3)
         w = wrng.integers(lo, hi, size=(K, 3, 3, C)).astype(np.float64)
+    elif x_dist == "normal_clip1":
+        w = _normal_in_unit(wrng, (K, 3, 3, C))
     else:
         w = wrng.standard_normal(size=(K, 3, 3, C)) * np.sqrt(2.0 / (9.0 * C))
     return x.astype(np.float32), w.astype(np.float32)

@@ -65,6 +65,13 @@ ALL_SHAPES = [
     ("0,-1,1,-1/2,2,1/2,-2,-1/4,4,1/4,-4,-3/4,4/3,inf", 12),        # t 14, alpha' 14
     ("0,-1,1,-1/2,2,1/2,-2,-1/4,4,1/4,-4,a^2+1,inf", 12),           # t 14, alpha' 15
     ("0,-1,1,-1/2,2,1/2,-2,-1/4,4,a^2+1,a^2-2,inf", 12),            # t 14, alpha' 16
+    # odd output tiles (separate path only): the tile sizes of Section 3.1's study
+    ("0,-1,1,-1/2,inf", 3),                                         # t 5, alpha' 5
+    ("0,-1,a^2+1,inf", 3),                                          # t 5, alpha' 6
+    ("0,-1,1,-1/2,2,1/2,inf", 5),                                   # t 7, alpha' 7
+    ("0,-1,1,-1/2,a^2+1,inf", 5),                                   # t 7, alpha' 8
+    ("0,-1,1,-1/2,2,1/2,-2,-1/4,inf", 7),                           # t 9, alpha' 9
+    ("0,-1,1,-1/2,2,1/2,a^2+1,inf", 7),                             # t 9, alpha' 10
 ]
 
 # smallest positive value of each storage type (the spacing of its subnormals)
@@ -157,3 +164,27 @@ def check_layer(p, op, x, w, dtype, y_gpu, label="", st=None):
     assert np.array_equal(to_np(Vg)[:, :, :C], Vo, equal_nan=True), f"{label}: V differs from the oracle"
     check_against_oracle(y_gpu, st, op, dtype, H, W, label)
     return st
+
+
+def pair_bound_1d(st, oplan, dtype, y_other, y_ref=None):
+    """``pair_bound`` for the 1D path (stages of winograd1d_emulated_stages):
+    the same argument with one output pass of alpha' fused multiply-adds."""
+    V, U, M = st["V"], st["U"], st["M"]
+    yo = st["y"] if y_ref is None else y_ref
+    al, C, K = V.shape[0], V.shape[-1], U.shape[1]
+    N, tl = V.shape[1:3]
+    m = oplan.n_o
+    Va = np.abs(V.reshape(al, -1, C).astype(np.float64))
+    Ua = np.abs(U.astype(np.float64))
+    Mabs = np.matmul(Va, np.transpose(Ua, (0, 2, 1)))
+    Mo = np.abs(M.reshape(al, -1, K).astype(np.float64))
+    u32 = 2.0 ** -24
+    dM = 2.2 * (C + 2) * u32 * Mabs
+    inner = (dM + 1.1 * (al + 1) * u32 * (2 * Mo + dM)).reshape(al, N, tl, K)
+    A = np.abs(np.array([[float(v) for v in r] for r in oplan.A]))
+    Y = np.einsum("ao,antk->ntok", A, inner, optimize=True).reshape(N, tl * m, K)
+    L = np.asarray(yo).shape[1]
+    D = 1.1 * Y[:, :L, :]
+    ud = 0.0 if dtype == "f32" else OF.UNIT_ROUNDOFF[dtype]
+    big = np.maximum(np.abs(np.asarray(yo, np.float64)), np.abs(np.asarray(y_other, np.float64)))
+    return D + 2.01 * ud * big + _TINY[dtype]

@@ -1,19 +1,22 @@
-"""The polynomial-set search on the GPU (Section 3.1's error-versus-ratio sweep
-on seeded synthetic data).
+"""The polynomial-set search on the GPU (Section 3.1's error-versus-ratio
+study on seeded synthetic data).
 
-* The search's reference, the fp32 F(2x2,3x3) plan, is within 1e-6 of fp64
-  direct convolution on the sweep data, so it can rank errors of 1e-6 and up.
-* Every set's GPU error obeys the parity rule against the oracle's emulation
-  of the same set (at most twice the oracle's same-algorithm error).
-* The paper's finding holds: for F(4x4) and F(6x6) the most accurate set with
-  degree-2 moduli is several times more accurate than the most accurate set
-  of linear points, in fp32 and in bf16.
-* Plan selection returns the most accurate candidate, or the fastest one
-  within an error cap.
+* The search's reference is the library's float64 direct convolution: equal
+  to the oracle's float64 convolution up to float64 summation order.
+* Every set's GPU error against it obeys the parity rule against the
+  oracle's emulation of the same set (at most twice the oracle's
+  same-algorithm error), in the layer sweep and in the X1 study (1D and 2D,
+  m = 2 .. 8, random one-tile convolutions with values in (-1, 1)).
+* The paper's finding, on our data: for F(4x4) and F(6x6) the most accurate
+  set with degree-2 moduli is several times more accurate than the most
+  accurate set of linear points, in fp32 and in bf16.
+* Plan selection on a layer's own input returns the most accurate candidate
+  (ties within 1% to the lower ratio), or the fastest one within an error cap.
 """
+from fractions import Fraction
+
 import numpy as np
 import pytest
-import torch
 
 from gpu_helpers import to_np
 from oracle import conv as OC
@@ -27,12 +30,13 @@ pytestmark = pytest.mark.gpu
 SHAPE = (1, 24, 24, 32, 32)
 
 
-def test_reference_is_accurate():
+def test_reference_is_float64_direct():
     for dtype in ("f32", "bf16"):
         x, w = S.layer_inputs(*SHAPE, dtype=dtype, seed=0)
-        ref = to_np(S.reference(x, w)).astype(np.float64)
+        ref = S.reference(x, w).cpu().numpy()
         x64, w64 = to_np(x).astype(np.float64), to_np(w).astype(np.float64)
-        assert OC.rel_l2(ref, OC.direct_f64(x64, w64)) < 1e-6
+        exact = OC.direct_f64(x64, w64)
+        assert np.max(np.abs(ref - exact)) <= 1e-13 * np.max(np.abs(exact))
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -40,14 +44,13 @@ def test_reference_is_accurate():
 def test_sweep_parity_and_superlinear_advantage(m, dtype):
     sets = S.candidate_sets(m, max_quadratic=2)
     print(f"[search] m={m} {dtype}: {len(sets)} sets", flush=True)
-    rows = S.sweep(sets, m, dtype, shape=SHAPE, seed=0)
+    rows = S.sweep(sets, m, dtype, shape=SHAPE, seeds=(0,))
     x, w = WL.draw_inputs(*SHAPE, "halfnormal", 0)
     x, w = OF.to_dtype(x, dtype), OF.to_dtype(w, dtype)
     y64 = OC.direct_f64(x, w)
     for r in rows:
         e_or = OC.rel_l2(OC.winograd_emulated(x, w, OP.build_plan(r.moduli, n_o=m), dtype), y64)
-        # the sweep's error is measured against the fp32 F(2x2) reference, itself ~1e-7 off
-        assert r.rel_l2 <= 2 * e_or + 2e-7, (r.moduli, r.rel_l2, e_or)
+        assert r.rel_l2 <= 2 * e_or, (r.moduli, r.rel_l2, e_or)
     best_lin = min(r.rel_l2 for r in rows if "a^2" not in r.moduli)
     best_quad = min(r.rel_l2 for r in rows if "a^2" in r.moduli)
     print(f"[search] m={m} {dtype}: best linear {best_lin:.2e}, best with quadratics {best_quad:.2e} "
@@ -56,14 +59,51 @@ def test_sweep_parity_and_superlinear_advantage(m, dtype):
     assert [r.rel_l2 for r in rows] == sorted(r.rel_l2 for r in rows)
 
 
+@pytest.mark.parametrize("dims", [1, 2])
+def test_x1_random_data_study(dims):
+    """Section 3.1: tiles 2..8, all-linear sets and sets with one of a^2+1,
+    a^2+a+1, a^2-a+1, fp32, errors against float64 direct convolution (here
+    1000 one-tile convolutions per set).  Each GPU error is at most twice the
+    oracle's emulation of the same set on the same inputs; the best set per
+    ratio is printed."""
+    recs = S.x1_experiment(dims=dims, m_values=range(2, 9), dtype="f32", loops=1000)
+    assert {r.m for r in recs} == set(range(2, 9))
+    for m in range(2, 9):
+        x, w = S.x1_inputs(dims, m, 1000, "f32", seed=m)
+        xa, wa = to_np(x), to_np(w)
+        if dims == 1:
+            xa, wa = xa[:, 0], wa[:, 0]
+            y64 = OC.direct1d_f64(xa, wa)
+        else:
+            y64 = OC.direct_f64(xa, wa)
+        for r in [r for r in recs if r.m == m]:
+            op = OP.build_plan(r.moduli, n_o=m)
+            yo = OC.winograd1d_emulated(xa, wa, op, "f32") if dims == 1 else OC.winograd_emulated(xa, wa, op, "f32")
+            e_or = OC.rel_l2(yo, y64)
+            assert r.rel_l2 <= 2 * e_or, (dims, r.moduli, r.rel_l2, e_or)
+    best = S.best_per_ratio(recs)
+    for (ratio, q), r in sorted(best.items(), key=lambda kv: (kv[0][0], kv[0][1])):
+        print(f"[x1] {dims}D ratio {float(ratio):.3f} quadratics {q} m={r.m} rel-L2 {r.rel_l2:.3e} "
+              f"tile-L2 {r.tile_l2:.3e} {{{r.moduli}}}", flush=True)
+    # Section 3.1: one quadratic beats Toom-Cook at ratios up to about 1.9 (1D)
+    # and 3.5 (2D), and not above.  The ratios where both kinds of set exist:
+    # 1D 1.5 (Toom-Cook m = 4, one quadratic m = 6) and 2 (m = 2, m = 3);
+    # 2D 2.25 (m = 4, m = 6) and 4 (m = 2, m = 3).
+    below, above = ((Fraction(3, 2), Fraction(2)) if dims == 1 else (Fraction(9, 4), Fraction(4)))
+    assert best[(below, 1)].rel_l2 < best[(below, 0)].rel_l2
+    assert best[(above, 0)].rel_l2 < best[(above, 1)].rel_l2
+
+
 def test_best_plan_policies():
     cands = WL.VGG_CANDIDATES
-    choice, rows = S.best_plan(28, 28, 64, 64, "bf16", cands, policy="accuracy")
-    assert choice == min(rows, key=lambda r: r[1])[0]
+    x, w = S.layer_inputs(2, 28, 28, 64, 64, "bf16", seed=0)
+    choice, rows = S.best_plan(x, w, cands, policy="accuracy")
+    lo = min(r[1] for r in rows)
+    assert [r for r in rows if r[0] == choice][0][1] <= 1.01 * lo
     cap = 3e-2
-    fast, rows = S.best_plan(28, 28, 64, 64, "bf16", cands, policy="speed", cap=cap, time_reps=3)
+    fast, rows = S.best_plan(x, w, cands, policy="speed", cap=cap, time_reps=3)
     ok = [r for r in rows if r[1] <= cap]
     assert fast in [r[0] for r in ok]
     assert all(np.isfinite(r[2]) for r in rows)
     with pytest.raises(ValueError):
-        S.best_plan(28, 28, 64, 64, "bf16", cands, policy="speed", cap=1e-9, time_reps=1)
+        S.best_plan(x, w, cands, policy="speed", cap=1e-9, time_reps=1)

@@ -40,3 +40,30 @@ def test_candidate_count_and_order():
     assert S.candidate_sets(4, max_quadratic=0) == [sets[0]]
     no_inf = S.candidate_sets(2, max_quadratic=0, with_inf=False)
     assert no_inf == ["0,-1,1,-1/2"]
+
+
+def test_x1_candidates_match_section_3_1():
+    """Section 3.1: linear points from the list 0, -1, 1, -1/2, 2, 1/2, -2,
+    -1/4, 4 and the quadratics a^2 + 1, a^2 + a + 1, a^2 - a + 1; every tile
+    from 2 to 8 (odd ones included) gives valid plans of compiled shapes."""
+    assert S.LINEAR_POINTS[:9] == ("0", "-1", "1", "-1/2", "2", "1/2", "-2", "-1/4", "4")
+    assert S.QUADRATICS_X1 == ("a^2+1", "a^2+a+1", "a^2-a+1")
+    for m in range(2, 9):
+        sets = S.candidate_sets(m, max_quadratic=1, quadratics=S.QUADRATICS_X1)
+        assert len(sets) == 4
+        for spec in sets:
+            p = Plan(spec, m=m, dtype="f32")
+            assert p.alpha == m + 2 + S.n_quadratics(spec)
+            p.close()
+
+
+def test_normal_restricted_to_unit_interval():
+    """The X1 draw: standard normal values restricted to (-1, 1)."""
+    import numpy as np
+    from paper_1905_05233_amd import workloads as WL
+    x, w = WL.draw_inputs(4, 16, 16, 8, 8, "normal_clip1", seed=0)
+    for a in (x, w):
+        assert np.all(np.abs(a) < 1)
+        assert abs(float(np.mean(a))) < 0.02
+        # the variance of N(0, 1) restricted to (-1, 1) is 1 - 2 phi(1) / (2 Phi(1) - 1) = 0.2911
+        assert abs(float(np.var(a)) - 0.2911) < 0.01
