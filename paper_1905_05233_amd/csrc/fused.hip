@@ -114,7 +114,10 @@ constexpr int vm_wait(int n) { return (n & 0xf) | (0x7 << 4) | (0xf << 8) | (((n
 // Bytes of that buffer: alpha'^2 x 32 tiles x (128 / K1)-byte rows.
 template <int ALPHA, int K1> constexpr int k1_vbuf_bytes() { return K1 ? ALPHA * ALPHA * 32 * (128 / K1) : 16; }
 
-template <int D, int MM, int ALPHA, int WT, bool NARROW, int K1>
+// ONE: every channel row fits one step (narrow rows, or rows of at most 128
+// bytes), so a step's MFMA results are M of its domain point and the
+// two-level channel sum is skipped.
+template <int D, int MM, int ALPHA, int WT, bool NARROW, int K1, bool ONE>
 __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
     const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, typename DTypeOf<D>::type* __restrict__ y,
     OutputTable tab, Geometry geo, int kw, int n_kb, int rb, int n_slices, int xp,
@@ -283,20 +286,25 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
         }
     };
     auto fold = [&]() __attribute__((always_inline)) {   // the step (a, bc, sl)
+        if constexpr (!ONE) {
 #pragma unroll
-        for (int w = 0; w < WT; ++w) acc[w] += part[w];
-        if (sl == n_slices - 1) {
+            for (int w = 0; w < WT; ++w) acc[w] += part[w];
+        }
+        if (ONE || sl == n_slices - 1) {
             // M[a][bc] of this block is complete: fold it into Z (pass 1)
+            const f32x4* mv = ONE ? part : acc;
 #pragma unroll
             for (int o = 0; o < MM; ++o) {
                 const float c = cz[o];
 #pragma unroll
                 for (int w = 0; w < WT; ++w)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) Z[w][o][r] = __builtin_fmaf(c, acc[w][r], Z[w][o][r]);
+                    for (int r = 0; r < 4; ++r) Z[w][o][r] = __builtin_fmaf(c, mv[w][r], Z[w][o][r]);
             }
+            if constexpr (!ONE) {
 #pragma unroll
-            for (int w = 0; w < WT; ++w) acc[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                for (int w = 0; w < WT; ++w) acc[w] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            }
             if (a == ALPHA - 1) {
                 // column bc done: pass 2 into the output tile
 #pragma unroll
@@ -558,11 +566,11 @@ struct CoArgs {
     unsigned nb;
 };
 
-template <int D, int TT, int A, int W, bool NAR, int K1>
+template <int D, int TT, int A, int W, bool NAR, int K1, bool ONE>
 hipError_t launch_co_instance(const CoArgs& c, hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
     if constexpr (k1_vbuf_bytes<A, K1>() <= 49152) {
-        hipLaunchKernelGGL((contract_output_kernel<D, TT - 2, A, W, NAR, K1>), dim3(c.nb), dim3(kThreads), 0, stream,
+        hipLaunchKernelGGL((contract_output_kernel<D, TT - 2, A, W, NAR, K1, ONE>), dim3(c.nb), dim3(kThreads), 0, stream,
                            c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.kw, c.n_kb, c.rb, c.n_slices, c.xp,
                            static_cast<const Elem*>(c.x), c.itab);
         return hipGetLastError();
@@ -607,10 +615,11 @@ hipError_t launch_co(const Geometry& g, const OutputTable& tab, const void* V, c
     c.nb = static_cast<unsigned>(grid);
 #define WG_CO_CASE(TT, A, W)                                                                              \
     if (g.t == TT && g.alpha == A && wt == W) {                                                           \
-        if (x && xp == 8) return launch_co_instance<D, TT, A, W, true, 8>(c, stream);                     \
-        if (x) return launch_co_instance<D, TT, A, W, true, 4>(c, stream);                                \
-        if (xp > 1) return launch_co_instance<D, TT, A, W, true, 0>(c, stream);                           \
-        return launch_co_instance<D, TT, A, W, false, 0>(c, stream);                                      \
+        if (x && xp == 8) return launch_co_instance<D, TT, A, W, true, 8, true>(c, stream);               \
+        if (x) return launch_co_instance<D, TT, A, W, true, 4, true>(c, stream);                          \
+        if (xp > 1) return launch_co_instance<D, TT, A, W, true, 0, true>(c, stream);                     \
+        if (c.n_slices == 1) return launch_co_instance<D, TT, A, W, false, 0, true>(c, stream);           \
+        return launch_co_instance<D, TT, A, W, false, 0, false>(c, stream);                               \
     }
     WG_CO_CASE(4, 4, 1) WG_CO_CASE(4, 5, 1) WG_CO_CASE(4, 6, 1) WG_CO_CASE(4, 7, 1)
     WG_CO_CASE(4, 4, 2) WG_CO_CASE(4, 5, 2) WG_CO_CASE(4, 6, 2) WG_CO_CASE(4, 7, 2)
