@@ -251,13 +251,18 @@ def residue_map(m, ncols, factor=None):
     return [[cols[j][i] for j in range(ncols)] for i in range(d)]
 
 
-def build_plan(moduli_spec, n_o, n_h=3, inner="0,-1,inf", factors="B"):
+def build_plan(moduli_spec, n_o, n_h=3, inner="0,-1,inf", factors="B", scaling="none"):
     """Build G^W, A^W, B^W exactly for F(n_o, n_h) from a modulus set.
 
     ``factors`` places the CRT factors N_i: "B" (the paper's matrices, inside
-    E) or "G" (multiplying the kernel residues)."""
+    E) or "G" (multiplying the kernel residues).  ``scaling`` "l1" applies the
+    diagonal scaling of G and A^T that Section 4 cites (Vincent et al.): each
+    domain row of G and of A divided by its 1-norm, B's column multiplied by
+    both, which leaves every domain row's rank-1 term unchanged."""
     if factors not in ("B", "G"):
         raise ValueError("factors must be 'B' or 'G'")
+    if scaling not in ("none", "l1"):
+        raise ValueError("scaling must be 'none' or 'l1'")
     finite, has_inf = parse_modulus_set(moduli_spec)
     inner_pts, inner_inf = parse_points(inner)
     n = n_h + n_o - 2
@@ -354,6 +359,16 @@ def build_plan(moduli_spec, n_o, n_h=3, inner="0,-1,inf", factors="B"):
         B = [EC[i] + [vM[i]] for i in range(n + 1)]
     else:
         B = EC
+
+    if scaling == "l1":
+        for x in range(len(G)):
+            # a zero row (a domain point the output never uses) stays as it is
+            sg = sum((abs(v) for v in G[x]), Fraction(0)) or Fraction(1)
+            sa = sum((abs(v) for v in A[x]), Fraction(0)) or Fraction(1)
+            G[x] = [v / sg for v in G[x]]
+            A[x] = [v / sa for v in A[x]]
+            for k in range(n + 1):
+                B[k][x] = B[k][x] * sg * sa
 
     plan.G, plan.A, plan.B = G, A, B
     plan.C, plan.E, plan.N, plan.M, plan.Mi = C, E, N, Mpoly, Mi

@@ -10,6 +10,7 @@ from fractions import Fraction
 import pytest
 
 from conftest import frac_matrix, load_golden
+from oracle import conv as OC
 from oracle import plan as OP
 from oracle import polynomials as P
 
@@ -361,3 +362,42 @@ def test_irreducible_cubics_accepted(poly):
     assert OP.is_irreducible(P.monic(P.parse(poly)))
     pl = OP.build_plan(f"0,-1,{poly},inf", n_o=4, inner="0,-1,1,-2,inf")
     assert OP.trilinear_defect(pl) == 0
+
+
+# ---------------------------------------------------------------------------
+# Diagonal scaling of G and A^T (scaling="l1")
+# ---------------------------------------------------------------------------
+
+def test_l1_scaling_of_f2x2_by_hand():
+    """{0, 1, -1, inf}: G rows [1,1,1] and [1,-1,1] have 1-norm 3, A rows
+    [1,1] and [1,-1] have 1-norm 2; those rows become thirds and halves and
+    the B columns 1 and 2 (B^T rows [0,1/2,1/2,0] and [0,-1/2,1/2,0]) are
+    multiplied by 6; rows 0 and 3 have norm 1 and stay."""
+    pl = OP.build_plan("0,1,-1,inf", n_o=2, scaling="l1")
+    t, h = Fraction(1, 3), Fraction(1, 2)
+    assert pl.G == [[1, 0, 0], [t, t, t], [t, -t, t], [0, 0, 1]]
+    assert pl.A == [[1, 0], [h, h], [h, -h], [0, 1]]
+    assert pl.BT == [[1, 0, -1, 0], [0, 3, 3, 0], [0, -3, 3, 0], [0, -1, 0, 1]]
+
+
+@pytest.mark.parametrize("spec,m,inner", [
+    ("0,1,-1,1/2,-1/2,inf", 4, "0,-1,inf"), ("0,1,-1,a^2+1,inf", 4, "0,-1,inf"),
+    ("0,-1,1,a^2+1,a^2-2,inf", 6, "0,-1,inf"), ("0,-1,1,-1/2,2,1/2,-2,-1/4,4,inf", 8, "0,-1,inf"),
+    ("a^2+1,a^2+2", 2, "0,-1,inf"), ("0,-1,a^3+2,inf", 4, "0,-1,1,-2,inf"),
+    ("0,a^3+2", 2, "0,-1,1,-2,inf"),    # its cubic block has a zero A row: left unscaled
+])
+def test_l1_scaling_keeps_each_rank_one_term(spec, m, inner):
+    """Scaling moves magnitude between the three factors of every domain
+    point's term A[xi] (x) G[xi] (x) B[:, xi], never the term itself; G and A
+    rows end with 1-norm 1; exact Winograd still equals direct convolution."""
+    pl = OP.build_plan(spec, n_o=m, inner=inner)
+    ps = OP.build_plan(spec, n_o=m, inner=inner, scaling="l1")
+    assert _triples(ps.G, ps.A, ps.BT) == _triples(pl.G, pl.A, pl.BT)
+    assert OP.trilinear_defect(ps) == 0
+    for row in ps.G + ps.A:
+        assert sum(abs(v) for v in row) in (0, 1)
+    x = [[[[Fraction((3 * i + 5 * j + c) % 7 - 3, 2) for c in range(2)] for j in range(m + 1)]
+          for i in range(m + 2)]]
+    w = [[[[Fraction((i - j + 2 * c + k) % 5 - 2) for c in range(2)] for j in range(3)] for i in range(3)]
+         for k in range(2)]
+    assert OC.winograd_exact(x, w, ps) == OC.direct_exact(x, w)
