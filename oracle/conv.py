@@ -219,6 +219,50 @@ def contraction_emulated(V, U):
     return M.reshape((al, al) + shp + (K,))
 
 
+def leaf_channels(dtype):
+    """Channels per leaf of the pairwise channel sum: 64 bytes of a channel
+    row (16 fp32, 32 fp16/bf16 values)."""
+    return 16 if dtype == "f32" else 32
+
+
+def contraction_emulated_pairwise(V, U, leaf):
+    """M[a, b, tiles, k] = sum_c V U with the channels summed pairwise (the
+    pairwise summation over channels that Section 4 names): leaves of
+    ``leaf`` consecutive channels, each summed in fp32, then the complete
+    binary tree over the leaves in channel order, the leaf list padded with
+    empty leaves to a power of two (an empty subtree passes its sibling
+    through unchanged), every addition rounded to fp32."""
+    al = V.shape[0]
+    shp = V.shape[2:-1]
+    C = V.shape[-1]
+    K = U.shape[2]
+    Vf = V.reshape(al, al, -1, C)
+    n = -(-C // leaf)
+    leaves = []
+    for i in range(n):
+        sl = slice(i * leaf, min(C, (i + 1) * leaf))
+        Mi = np.empty((al, al, Vf.shape[2], K), dtype=np.float32)
+        for a in range(al):
+            for b in range(al):
+                Mi[a, b] = Vf[a, b, :, sl] @ U[a, b, :, sl].T
+        leaves.append(Mi)
+    size = 1
+    while size < n:
+        size *= 2
+    leaves += [None] * (size - n)
+
+    def tree(lo, hi):
+        if hi - lo == 1:
+            return leaves[lo]
+        mid = (lo + hi) // 2
+        left, right = tree(lo, mid), tree(mid, hi)
+        if right is None:
+            return left
+        return (left + right).astype(np.float32)
+
+    return tree(0, size).reshape((al, al) + shp + (K,))
+
+
 def output_transform_emulated(M, plan, dtype, H, W, mats=None):
     """y = round_dtype(A^T M A) in fp32, cropped to H x W, NHWC."""
     _, A, _ = mats or plan_f32(plan)
@@ -232,10 +276,11 @@ def output_transform_emulated(M, plan, dtype, H, W, mats=None):
     return np.ascontiguousarray(y[:, :H, :W, :])
 
 
-def winograd_emulated_stages(x, w, plan, dtype):
+def winograd_emulated_stages(x, w, plan, dtype, channel_sum="mfma"):
     """Full layer by eq. (2) with the library's rounding points (see module
     doc), returning every stage: U [al][al][K][C], V [al][al][N][th][tw][C],
-    M [al][al][N][th][tw][K] (fp32) and y [N][H][W][K].
+    M [al][al][N][th][tw][K] (fp32) and y [N][H][W][K].  ``channel_sum``
+    "pairwise" sums M's channels pairwise (contraction_emulated_pairwise).
 
     ``x`` and ``w`` must already hold values representable in ``dtype``.
     """
@@ -245,7 +290,10 @@ def winograd_emulated_stages(x, w, plan, dtype):
     mats = plan_f32(plan)
     U = kernel_transform_emulated(w, plan, dtype, mats)
     V = input_transform_emulated(x, plan, dtype, mats)
-    M = contraction_emulated(V, U)
+    if channel_sum == "pairwise":
+        M = contraction_emulated_pairwise(V, U, leaf_channels(dtype))
+    else:
+        M = contraction_emulated(V, U)
     y = output_transform_emulated(M, plan, dtype, x.shape[1], x.shape[2], mats)
     return {"U": U, "V": V, "M": M, "y": y}
 

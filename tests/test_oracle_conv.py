@@ -155,3 +155,40 @@ def test_rel_l2():
     a = np.array([3.0, 4.0])
     assert OC.rel_l2(a, a) == 0.0
     assert OC.rel_l2(np.array([3.0, 4.0 + 5.0]), a) == pytest.approx(1.0)
+
+
+def test_pairwise_contraction_tree_shape():
+    """The pairwise channel sum of the oracle against hand-built trees: with
+    leaf = 1 channel and values chosen so that fp32 addition order shows,
+    5 leaves sum as ((l0 + l1) + (l2 + l3)) + l4 (padded to 8 leaves) and 3
+    as (l0 + l1) + l2; the plain left-to-right sum differs."""
+    big, tiny = np.float32(2.0 ** 24), np.float32(1.0)
+    for vals, want in (([big, tiny, tiny, tiny, -big], np.float32((big + tiny) + (tiny + tiny)) + (-big)),
+                       ([big, tiny, tiny], np.float32(big + tiny) + tiny)):
+        C = len(vals)
+        V = np.array(vals, np.float32).reshape(1, 1, 1, C)
+        U = np.ones((1, 1, 1, C), np.float32)
+        got = OC.contraction_emulated_pairwise(V, U, leaf=1)
+        assert got.shape == (1, 1, 1, 1)
+        assert got[0, 0, 0, 0] == np.float32(want)
+    seq = np.float32(0)
+    for v in [big, tiny, tiny, tiny, -big]:
+        seq = np.float32(seq + v)
+    assert seq != OC.contraction_emulated_pairwise(np.array([big, tiny, tiny, tiny, -big], np.float32)
+                                                   .reshape(1, 1, 1, 5), np.ones((1, 1, 1, 5), np.float32), 1)[0, 0, 0, 0]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_pairwise_contraction_close_to_exact_sum(dtype):
+    """On random data the pairwise sum differs from the exact channel sum by
+    at most its bound (leaf + ceil(log2 leaves) + 2) u32 sum |V||U|."""
+    rng = np.random.default_rng(2)
+    C, leaf = 300, OC.leaf_channels(dtype)
+    V = OF.to_dtype(rng.standard_normal((2, 2, 7, C)).astype(np.float32), dtype)
+    U = OF.to_dtype(rng.standard_normal((2, 2, 5, C)).astype(np.float32), dtype)
+    M = OC.contraction_emulated_pairwise(V, U, leaf).astype(np.float64)
+    ex = np.einsum("abtc,abkc->abtk", V.astype(np.float64), U.astype(np.float64))
+    mag = np.einsum("abtc,abkc->abtk", np.abs(V).astype(np.float64), np.abs(U).astype(np.float64))
+    n = -(-C // leaf)
+    depth = (n - 1).bit_length()
+    assert np.all(np.abs(M - ex) <= 1.1 * (leaf + depth + 2) * 2.0 ** -24 * mag)
