@@ -131,18 +131,41 @@ typedef enum { WG_FACTORS_IN_B = 0, WG_FACTORS_IN_G = 1 } wg_crt_factors;
  * order. */
 typedef enum { WG_PATH_AUTO = 0, WG_PATH_SEPARATE = 1, WG_PATH_FUSED = 2, WG_PATH_FUSED_INPUT = 3 } wg_conv_path;
 
+/* Diagonal scaling of the transforms (the scaling of G and A^T that the
+ * related work of Section 4 cites from Vincent et al.).  WG_SCALE_NONE keeps
+ * the matrices of Algorithms 1 and 2.  WG_SCALE_ROWS_L1 divides every domain
+ * row of G and of A by its 1-norm (sum of absolute values; a zero row stays
+ * as it is) and multiplies the matching column of B by both norms: each
+ * domain point's rank-1 term
+ * B[:, xi] G[xi] A[xi] is unchanged, so the algorithm stays exact and only
+ * its roundings change. */
+typedef enum { WG_SCALE_NONE = 0, WG_SCALE_ROWS_L1 = 1 } wg_scaling;
+
 /* generic_transforms = 1 keeps a plan on the transform kernels that read its
  * coefficients at run time even when its tables equal a built-in plan's (see
  * winograd_plan_builtin); 0 (the default) lets it use the built-in kernels. */
+/* How the contraction sums over the input channels.  WG_SUM_MFMA: the
+ * matrix cores' accumulation chains (the fast kernels).  WG_SUM_PAIRWISE: the
+ * pairwise summation over channels that the related work of Section 4 names
+ * (after Barabasz et al. 2018): each 64-byte piece of a channel row (16 fp32
+ * or 32 fp16/bf16 channels) is summed into its own fp32 partial, and the
+ * partials are added in a binary tree in channel order, so the rounding
+ * error of the sum grows with log2 C rather than C.  It runs on the separate
+ * path with a slower kernel (fragments from memory, nothing staged). */
+typedef enum { WG_SUM_MFMA = 0, WG_SUM_PAIRWISE = 1 } wg_channel_sum;
+
 typedef struct {
     wg_crt_factors factors;
     wg_conv_path path;
     int generic_transforms;
+    wg_scaling scaling;
+    wg_channel_sum channel_sum;
 } wg_plan_options;
 
 /* winograd_plan_create_str with options (opts == NULL means all defaults:
- * WG_FACTORS_IN_B, WG_PATH_AUTO, generic_transforms 0).  An unknown option
- * value is WG_ERR_ARG. */
+ * WG_FACTORS_IN_B, WG_PATH_AUTO, generic_transforms 0, WG_SCALE_NONE,
+ * WG_SUM_MFMA).  An unknown option value is WG_ERR_ARG, and so is
+ * WG_SUM_PAIRWISE with a fused path. */
 wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, int r, wg_dtype dtype,
                                   const wg_plan_options* opts, wg_plan* out);
 
@@ -266,7 +289,7 @@ wg_status winograd_kernel_input_transform(wg_plan plan, const wg_tensor* w, cons
 
 /* M[xi][t][k] = sum_c V[xi][t][c] U[xi][k][c]: alpha'^2 GEMMs [T x C][C x K]
  * on the matrix cores with fp32 accumulation (the Hadamard product of eq. (2)
- * summed over input channels).  The kernels address 128 rows of V or U with
+ * summed over input channels), in the plan's channel-sum order.  The kernels address 128 rows of V or U with
  * 32-bit offsets: a channel row (Cp storage elements) of 33,553,920 bytes
  * (just under 32 MiB) or more, or
  * more than 2^31 - 1 blocks of 128 x 128, fails with WG_ERR_HIP ("invalid

@@ -28,10 +28,13 @@ class WgPolySet(ctypes.Structure):
 
 
 class WgPlanOptions(ctypes.Structure):
-    _fields_ = [("factors", ctypes.c_int), ("path", ctypes.c_int), ("generic_transforms", ctypes.c_int)]
+    _fields_ = [("factors", ctypes.c_int), ("path", ctypes.c_int), ("generic_transforms", ctypes.c_int),
+                ("scaling", ctypes.c_int), ("channel_sum", ctypes.c_int)]
 
 
 FACTOR_CODES = {"B": 0, "G": 1}
+SCALING_CODES = {"none": 0, "l1": 1}
+CHANNEL_SUM_CODES = {"mfma": 0, "pairwise": 1}
 PATH_CODES = {"auto": 0, "separate": 1, "fused": 2, "fused_input": 3}
 PATH_NAMES = {v: k for k, v in PATH_CODES.items()}
 

@@ -40,6 +40,7 @@ UNITS = [
     ("fused.hip", DEVICE + ["-DWG_DTYPE=2"], "fused_bf16.o"),
     ("layer_ops.hip", DEVICE, "layer_ops.o"),
     ("conv1d.hip", DEVICE, "conv1d.o"),
+    ("contract_pairwise.hip", DEVICE, "contract_pairwise.o"),
 ]
 
 

@@ -28,6 +28,7 @@ struct wg_plan_s {
     int dtype = 0;
     int path = WG_PATH_AUTO;
     int builtin = -1;   // id of the built-in plan with the same fp32 tables, or -1
+    int channel_sum = WG_SUM_MFMA;
     void* ws = nullptr;
     size_t ws_bytes = 0;
     wg::InputTable itab{};
@@ -151,6 +152,7 @@ bool input_fused_supported(int dt, const wg::Geometry& g) {
 // the fused kernel (its prologue runs the transform with run-time
 // coefficients, serialised ahead of each block's contraction).
 int resolve_path(const wg_plan_s* p, const wg::Geometry& g) {
+    if (p->channel_sum == WG_SUM_PAIRWISE) return WG_PATH_SEPARATE;   // the fused kernels chain on MFMA
     const bool ok = fused_supported(p->dtype, g);
     if (p->path == WG_PATH_FUSED_INPUT) return ok && input_fused_supported(p->dtype, g) ? WG_PATH_FUSED_INPUT : -1;
     if (p->path == WG_PATH_FUSED) return ok ? WG_PATH_FUSED : -1;
@@ -251,7 +253,15 @@ hipError_t launch_it(int dt, const wg::Geometry& g, const wg::InputTable& t, con
         default: return wg::launch_input_transform_t<2>(g, t, x, V, bi, s);
     }
 }
-hipError_t launch_ct(int dt, const wg::Geometry& g, const void* V, const void* U, float* M, hipStream_t s) {
+hipError_t launch_ct(int dt, const wg::Geometry& g, const void* V, const void* U, float* M, hipStream_t s,
+                     int channel_sum = WG_SUM_MFMA) {
+    if (channel_sum == WG_SUM_PAIRWISE) {
+        switch (dt) {
+            case 0: return wg::launch_contract_pairwise_t<0>(g, V, U, M, s);
+            case 1: return wg::launch_contract_pairwise_t<1>(g, V, U, M, s);
+            default: return wg::launch_contract_pairwise_t<2>(g, V, U, M, s);
+        }
+    }
     switch (dt) {
         case 0: return wg::launch_contract_t<0>(g, V, U, M, s);
         case 1: return wg::launch_contract_t<1>(g, V, U, M, s);
@@ -355,14 +365,23 @@ wg_status winograd_plan_create_ex(const char* moduli, const char* inner, int m, 
             return fail(WG_ERR_ARG, "unknown convolution path");
         const int generic = opts ? opts->generic_transforms : 0;
         if (generic != 0 && generic != 1) return fail(WG_ERR_ARG, "generic_transforms must be 0 or 1");
+        const int scaling = opts ? static_cast<int>(opts->scaling) : WG_SCALE_NONE;
+        if (scaling != WG_SCALE_NONE && scaling != WG_SCALE_ROWS_L1) return fail(WG_ERR_ARG, "unknown scaling");
+        const int csum = opts ? static_cast<int>(opts->channel_sum) : WG_SUM_MFMA;
+        if (csum != WG_SUM_MFMA && csum != WG_SUM_PAIRWISE) return fail(WG_ERR_ARG, "unknown channel sum");
+        if (csum == WG_SUM_PAIRWISE && (path == WG_PATH_FUSED || path == WG_PATH_FUSED_INPUT))
+            return fail(WG_ERR_ARG, "pairwise channel sums run on the separate path only");
         const std::vector<wg::Modulus> mods = wg::parse_moduli(moduli);
         std::vector<wg::Rat> pts;
         bool inf = true;
         if (inner && inner[0] != '\0') wg::parse_points(inner, &pts, &inf);
         else pts = {wg::Rat(0), wg::Rat(-1)};
-        s = finish_plan(wg::build_transforms(mods, pts, inf, m, r, factors == WG_FACTORS_IN_G), dtype, out);
+        s = finish_plan(wg::build_transforms(mods, pts, inf, m, r, factors == WG_FACTORS_IN_G,
+                                             scaling == WG_SCALE_ROWS_L1),
+                        dtype, out);
         if (s == WG_OK) {
             (*out)->path = path;
+            (*out)->channel_sum = csum;
             if (generic) (*out)->builtin = -1;
         }
         return s;
@@ -494,7 +513,7 @@ wg_status conv2d_with(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_t
     if (s != WG_OK) return s;
     if (L.path == WG_PATH_FUSED)
         return from_hip(launch_co(dt, L.g, plan->otab, V, U, y->data, stream), "fused contraction");
-    if ((s = from_hip(launch_ct(dt, L.g, V, U, M, stream), "contraction")) != WG_OK) return s;
+    if ((s = from_hip(launch_ct(dt, L.g, V, U, M, stream, plan->channel_sum), "contraction")) != WG_OK) return s;
     return from_hip(launch_ot(dt, L.g, plan->otab, M, y->data, plan->builtin, stream), "output transform");
 }
 
@@ -559,7 +578,8 @@ wg_status winograd_conv1d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, 
         default: e = wg::launch_input_transform_1d_t<2>(L.g, plan->itab, x->data, V, stream); break;
     }
     if ((s = from_hip(e, "1D input transform")) != WG_OK) return s;
-    if ((s = from_hip(launch_ct(plan->dtype, L.g, V, U, M, stream), "contraction")) != WG_OK) return s;
+    if ((s = from_hip(launch_ct(plan->dtype, L.g, V, U, M, stream, plan->channel_sum), "contraction")) != WG_OK)
+        return s;
     switch (plan->dtype) {
         case 0: e = wg::launch_output_transform_1d_t<0>(L.g, plan->otab, M, y->data, stream); break;
         case 1: e = wg::launch_output_transform_1d_t<1>(L.g, plan->otab, M, y->data, stream); break;
@@ -627,7 +647,7 @@ wg_status winograd_contract(wg_plan plan, const void* V, const void* U, float* M
     if (!dims_ok(T, 1, 1, C, K)) return fail(WG_ERR_ARG, "sizes must be in [1, 2^31)");
     wg::Geometry g = wg::make_geometry(1, 1, 1, C, K, plan->tr.m, plan->tr.alpha);
     g.T = T;
-    return from_hip(launch_ct(plan->dtype, g, V, U, M, stream), "contraction");
+    return from_hip(launch_ct(plan->dtype, g, V, U, M, stream, plan->channel_sum), "contraction");
 }
 
 wg_status winograd_output_transform(wg_plan plan, const float* M, wg_tensor* y, hipStream_t stream) {

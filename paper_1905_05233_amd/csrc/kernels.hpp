@@ -99,6 +99,11 @@ hipError_t launch_output_transform_t(const Geometry& g, const OutputTable& tab, 
 template <int D>
 hipError_t launch_contract_t(const Geometry& g, const void* V, const void* U, float* M, hipStream_t stream);
 
+// The same contraction with the channels summed pairwise (contract_pairwise.hip):
+// leaves of 64 bytes of each channel row, added in a binary tree.
+template <int D>
+hipError_t launch_contract_pairwise_t(const Geometry& g, const void* V, const void* U, float* M, hipStream_t stream);
+
 // Contraction fused with the output transform: V, U -> y with no M in memory.
 // Supported for input tiles up to 8 (m <= 6) and planes addressable with
 // 32-bit offsets; the launcher returns hipErrorInvalidValue otherwise.

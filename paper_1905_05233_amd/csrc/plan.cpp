@@ -266,7 +266,7 @@ void parse_points(const std::string& text, std::vector<Rat>* pts, bool* with_inf
 }
 
 Transforms build_transforms(const std::vector<Modulus>& moduli_in, const std::vector<Rat>& inner_pts,
-                            bool inner_inf, int m, int r, bool factors_in_g) {
+                            bool inner_inf, int m, int r, bool factors_in_g, bool scale_rows) {
     if (m < 1 || r < 1) throw PlanError(kErrArg, "tile sizes must be positive");
     const int n = m + r - 2;  // degree of the product polynomial s(a)
     std::vector<Poly> mods;
@@ -383,6 +383,29 @@ Transforms build_transforms(const std::vector<Modulus>& moduli_in, const std::ve
         ++col0;
     }
     if (col0 != alpha) throw PlanError(kErrInternal, "inconsistent domain size");
+
+    // scale_rows: every domain row of G and of A divided by its 1-norm, the
+    // matching column of B multiplied by both norms.  Each domain row's
+    // rank-1 term B[:, xi] G[xi] A[xi] is unchanged, so the algorithm stays
+    // exact; only the roundings move (the diagonal scaling of G and A^T that
+    // the related work of Section 4 cites).
+    if (scale_rows) {
+        auto absr = [](const Rat& v) { return v.num() < 0 ? -v : v; };
+        for (int x = 0; x < alpha; ++x) {
+            Rat sg(0), sa(0);
+            for (const Rat& v : G[static_cast<size_t>(x)]) sg += absr(v);
+            for (const Rat& v : A[static_cast<size_t>(x)]) sa += absr(v);
+            // a zero row (a domain point the output never uses) stays as it is
+            if (sg.is_zero()) sg = Rat(1);
+            if (sa.is_zero()) sa = Rat(1);
+            for (Rat& v : G[static_cast<size_t>(x)]) v = v / sg;
+            for (Rat& v : A[static_cast<size_t>(x)]) v = v / sa;
+            for (int row = 0; row < rowsB; ++row) {
+                Rat& b = B[static_cast<size_t>(row)][static_cast<size_t>(x)];
+                b = b * sg * sa;
+            }
+        }
+    }
 
     // ---- exact self-check: sum_xi B[k][xi] G[xi][i] A[xi][j] == [k == i+j] ----
     for (int k = 0; k < rowsB; ++k)

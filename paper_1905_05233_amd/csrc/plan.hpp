@@ -42,8 +42,9 @@ void parse_points(const std::string& text, std::vector<Rat>* pts, bool* with_inf
 
 // Algorithms 1 and 2 for F(m x m, r x r) plus the exact reconstruction check.
 // factors_in_g moves the CRT factors N_i of eq. (1) from B (the paper's
-// matrices) to the kernel transform G.
+// matrices) to the kernel transform G; scale_rows divides every domain row of
+// G and of A by its 1-norm and compensates in B.
 Transforms build_transforms(const std::vector<Modulus>& moduli, const std::vector<Rat>& inner_pts,
-                            bool inner_inf, int m, int r, bool factors_in_g = false);
+                            bool inner_inf, int m, int r, bool factors_in_g = false, bool scale_rows = false);
 
 }  // namespace wg

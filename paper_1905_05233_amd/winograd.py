@@ -38,29 +38,40 @@ class Plan:
     """A Winograd plan F(m x m, 3 x 3) built from a modulus set (Algorithms 1, 2)."""
 
     def __init__(self, moduli, m, dtype="f32", inner="0,-1,inf", r=3, factors="B", path="auto",
-                 generic_transforms=False):
+                 generic_transforms=False, scaling="none", channel_sum="mfma"):
         """``factors``: where the CRT factors N_i go, "B" (the paper's
         matrices) or "G" (on the kernel residues).  ``path``: "separate"
         (M through memory), "fused" (contraction and output transform in one
         kernel) or "auto" (chosen per layer shape).  ``generic_transforms``:
-        never use the built-in constant-coefficient transform kernels."""
+        never use the built-in constant-coefficient transform kernels.
+        ``scaling``: "none" or "l1" (every domain row of G and A divided by
+        its 1-norm, compensated in B).  ``channel_sum``: "mfma" (the matrix
+        cores' chains) or "pairwise" (a binary tree over 64-byte pieces of the
+        channel rows; separate path)."""
         if dtype not in N.DTYPE_CODES:
             raise ValueError(f"dtype must be one of {list(N.DTYPE_CODES)}")
         if factors not in N.FACTOR_CODES:
             raise ValueError(f"factors must be one of {list(N.FACTOR_CODES)}")
         if path not in N.PATH_CODES:
             raise ValueError(f"path must be one of {list(N.PATH_CODES)}")
+        if scaling not in N.SCALING_CODES:
+            raise ValueError(f"scaling must be one of {list(N.SCALING_CODES)}")
+        if channel_sum not in N.CHANNEL_SUM_CODES:
+            raise ValueError(f"channel_sum must be one of {list(N.CHANNEL_SUM_CODES)}")
         self._lib = N.lib()
         self._h = ctypes.c_void_p()
-        if factors == "B" and path == "auto" and not generic_transforms:
+        if factors == "B" and path == "auto" and not generic_transforms and scaling == "none" \
+                and channel_sum == "mfma":
             N.check(self._lib.winograd_plan_create_str(moduli.encode(), (inner or "").encode(), int(m), int(r),
                                                        N.DTYPE_CODES[dtype], ctypes.byref(self._h)))
         else:
-            opts = N.WgPlanOptions(N.FACTOR_CODES[factors], N.PATH_CODES[path], 1 if generic_transforms else 0)
+            opts = N.WgPlanOptions(N.FACTOR_CODES[factors], N.PATH_CODES[path], 1 if generic_transforms else 0,
+                                   N.SCALING_CODES[scaling], N.CHANNEL_SUM_CODES[channel_sum])
             N.check(self._lib.winograd_plan_create_ex(moduli.encode(), (inner or "").encode(), int(m), int(r),
                                                       N.DTYPE_CODES[dtype], ctypes.byref(opts),
                                                       ctypes.byref(self._h)))
         self.moduli, self.inner, self.dtype, self.factors, self.path = moduli, inner, dtype, factors, path
+        self.scaling, self.channel_sum = scaling, channel_sum
         vals = [ctypes.c_int() for _ in range(5)]
         N.check(self._lib.winograd_plan_info(self._h, *[ctypes.byref(v) for v in vals]))
         self.m, self.r, self.alpha, self.tile_in, _ = [v.value for v in vals]

@@ -87,7 +87,7 @@ def stages_on_device_layout(st):
     return U, V
 
 
-def pair_bound(st, oplan, dtype, y_other, H, W, y_ref=None):
+def pair_bound(st, oplan, dtype, y_other, H, W, y_ref=None, sum_terms=None):
     """Element-wise bound on |y_other - y_oracle| for another evaluation of
     eq. (2) with the library's rounding points that holds the same U and V
     bit for bit (the tests check that first, stage by stage).
@@ -110,6 +110,8 @@ def pair_bound(st, oplan, dtype, y_other, H, W, y_ref=None):
     ``y_ref`` replaces the oracle's y by a third evaluation with the same U
     and V (two GPU paths compared with each other): the same argument holds,
     since each path's M is within 1.1 (C + 2) u32 Mabs of the exact sum.
+    ``sum_terms`` replaces C + 2 for sums of another depth (pairwise sums:
+    leaf + ceil(log2 leaves) + 2).
     """
     V, U, M = st["V"], st["U"], st["M"]
     yo = st["y"] if y_ref is None else y_ref
@@ -123,7 +125,7 @@ def pair_bound(st, oplan, dtype, y_other, H, W, y_ref=None):
     Mabs = np.matmul(Va, np.transpose(Ua, (0, 2, 1)))
     Mo = np.abs(M.reshape(al * al, -1, K).astype(np.float64))
     u32 = 2.0 ** -24
-    dM = 2.2 * (C + 2) * u32 * Mabs
+    dM = 2.2 * ((C + 2) if sum_terms is None else sum_terms) * u32 * Mabs
     inner = (dM + 1.1 * (2 * al + 2) * u32 * (2 * Mo + dM)).reshape(al, al, N, th, tw, K)
     A = np.abs(np.array([[float(v) for v in r] for r in oplan.A]))
     Y = np.einsum("ao,abnxyk,bp->nxoypk", A, inner, A, optimize=True).reshape(N, th * m, tw * m, K)
@@ -133,12 +135,12 @@ def pair_bound(st, oplan, dtype, y_other, H, W, y_ref=None):
     return D + 2.01 * ud * big + _TINY[dtype]
 
 
-def check_against_oracle(y, st, oplan, dtype, H, W, label=""):
+def check_against_oracle(y, st, oplan, dtype, H, W, label="", sum_terms=None):
     """Assert |y - y_oracle| <= pair_bound element by element; print how
     tight the bound is (median bound / |y| and the largest error / bound)."""
     y = np.asarray(y, np.float64)
     yo = np.asarray(st["y"], np.float64)
-    b = pair_bound(st, oplan, dtype, y, H, W)
+    b = pair_bound(st, oplan, dtype, y, H, W, sum_terms=sum_terms)
     err = np.abs(y - yo)
     nz = np.abs(yo) > 0
     med = float(np.median(b[nz] / np.abs(yo[nz]))) if np.any(nz) else 0.0
@@ -149,7 +151,7 @@ def check_against_oracle(y, st, oplan, dtype, H, W, label=""):
     return med, worst
 
 
-def check_layer(p, op, x, w, dtype, y_gpu, label="", st=None):
+def check_layer(p, op, x, w, dtype, y_gpu, label="", st=None, sum_terms=None):
     """The GPU layer against the oracle's same-algorithm evaluation, element
     by element and tight: the plan's transform kernels (run here through
     the stage entry point that conv2d's first launch uses) give U and V equal
@@ -162,7 +164,7 @@ def check_layer(p, op, x, w, dtype, y_gpu, label="", st=None):
     Uo, Vo = stages_on_device_layout(st)
     assert np.array_equal(to_np(Ug)[:, :, :C], Uo, equal_nan=True), f"{label}: U differs from the oracle"
     assert np.array_equal(to_np(Vg)[:, :, :C], Vo, equal_nan=True), f"{label}: V differs from the oracle"
-    check_against_oracle(y_gpu, st, op, dtype, H, W, label)
+    check_against_oracle(y_gpu, st, op, dtype, H, W, label, sum_terms=sum_terms)
     return st
 
 

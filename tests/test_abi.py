@@ -74,6 +74,31 @@ def test_factors_in_g_plan_parity_with_oracle(spec, m, inner):
         assert np.array_equal(ours.view(np.uint32), want.view(np.uint32)), which
 
 
+@pytest.mark.parametrize("spec,m,inner", PLAN_SETS[1::2])
+@pytest.mark.parametrize("factors", ["B", "G"])
+def test_scaled_plan_parity_with_oracle(spec, m, inner, factors):
+    """WG_SCALE_ROWS_L1: exact matrices and fp32 tables equal the oracle's
+    scaling="l1" construction (with either CRT factor placement)."""
+    ref = OP.build_plan(spec, n_o=m, inner=inner, factors=factors, scaling="l1")
+    p = Plan(spec, m=m, dtype="f32", inner=inner, factors=factors, scaling="l1")
+    assert p.builtin == -1 or factors == "B"
+    for which, mat in (("G", ref.G), ("A", ref.A), ("B", ref.B)):
+        assert p.matrix(which) == mat
+        ours = np.array(p.matrix_f32(which), dtype=np.float32)
+        want = np.array([[OF.fraction_to_f32(v) for v in row] for row in mat], dtype=np.float32)
+        assert np.array_equal(ours.view(np.uint32), want.view(np.uint32)), which
+
+
+def test_unknown_scaling_rejected():
+    lib = N.lib()
+    bad = N.WgPlanOptions(0, 0, 0, 5)
+    h = ctypes.c_void_p()
+    assert lib.winograd_plan_create_ex(WL.F4_LINEAR.encode(), b"", 4, 3, 0, ctypes.byref(bad), ctypes.byref(h)) == 1
+    assert not h.value
+    with pytest.raises(ValueError):
+        Plan(WL.F4_LINEAR, m=4, scaling="l2")
+
+
 def test_create_ex_defaults_and_errors():
     lib = N.lib()
     h = ctypes.c_void_p()
@@ -243,7 +268,8 @@ def test_workspace_bytes_and_errors():
 
 def test_unsupported_kernel_shape_reported_at_launch():
     """A valid plan whose (tile, alpha') has no compiled kernel fails cleanly."""
-    p = Plan("0,1,-1,1/2,inf", m=3)      # tile 5: odd m has no transform kernels
+    p = Plan("a^2+1,a^2-2,inf", m=3)     # tile 5 with alpha' 7: no compiled transform kernels
+    assert (p.tile_in, p.alpha) == (5, 7)
     lib = N.lib()
     fake = ctypes.c_void_p(1 << 20)
     x = N.WgTensor(fake, 1, 8, 8, 4)

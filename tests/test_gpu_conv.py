@@ -142,3 +142,32 @@ def test_factors_in_g_bit_exact_dyadic():
     assert np.array_equal(OC.winograd_emulated(x, w, op, "f32").astype(np.float64), ref)
     y = to_np(Plan(WL.F2_LINEAR, m=2, dtype="f32", factors="G").conv2d(to_dev(x, "f32"), to_dev(w, "f32")))
     assert np.array_equal(y.astype(np.float64), ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("spec,m", [(WL.F4_LINEAR, 4), (WL.F4_A2P1, 4), (WL.F6_TWO_QUAD, 6),
+                                    ("0,-1,1,-1/2,2,1/2,-2,-1/4,4,inf", 8)])
+@pytest.mark.parametrize("path", ["separate", "fused"])
+def test_scaled_plan_parity(spec, m, dtype, path):
+    """Plans with the rows of G and A scaled to unit 1-norm (compensated in
+    B): U and V bit-equal to the oracle's emulation of the scaled plan, y
+    within the pair bound, and the 2x rule against fp64 direct convolution.
+    In fp16 the scaling keeps F(8x8)'s transforms in range (rel-L2 about 0.07
+    where the unscaled plan overflows)."""
+    from paper_1905_05233_amd.winograd import Plan
+    if path == "fused" and m > 6:
+        pytest.skip("the fused kernel takes input tiles up to 8")
+    N, H, W, C, K = 2, 26, 30, 24, 40
+    x, w = WL.draw_inputs(N, H, W, C, K, "halfnormal", seed=9 * m)
+    x, w = OF.to_dtype(x, dtype), OF.to_dtype(w, dtype)
+    op = OP.build_plan(spec, n_o=m, scaling="l1")
+    p = Plan(spec, m=m, dtype=dtype, scaling="l1", path=path)
+    y = to_np(p.conv2d(to_dev(x, dtype), to_dev(w, dtype))).astype(np.float64)
+    st = check_layer(p, op, x, w, dtype, y, label=f"scaled {spec} {dtype} {path}")
+    y64 = OC.direct_f64(x, w)
+    err_gpu, err_or = OC.rel_l2(y, y64), OC.rel_l2(st["y"], y64)
+    err_plain = OC.rel_l2(OC.winograd_emulated(x, w, OP.build_plan(spec, n_o=m), dtype), y64)
+    print(f"[scaled] {spec} {dtype} {path}: gpu {err_gpu:.3e} oracle {err_or:.3e} (unscaled oracle {err_plain:.3e})",
+          flush=True)
+    assert np.all(np.isfinite(y))
+    assert err_gpu <= 2 * err_or
