@@ -245,6 +245,30 @@ def run_vgg(a):
     _, trace = stack.forward(x, keep=True)
     torch.cuda.synchronize()
 
+    if a.profile_kernel == "each":
+        # every stage kernel of every layer, --steps launches each, in order
+        order = []
+        for li, (L, (xi, yi)) in enumerate(zip(stack.layers, trace)):
+            y = torch.empty_like(yi)
+            stages = make_stages(L["plan"], xi, L["w"], y, N, L["hw"], L["hw"], L["C"], L["K"], stream)
+            for fn in stages.values():
+                NAT.check(fn())
+            torch.cuda.synchronize()
+            work = _vgg_layer_work(L, N, dtype)
+            for name, fn in stages.items():
+                for _ in range(a.steps):
+                    NAT.check(fn())
+                torch.cuda.synchronize()
+                per = 2 if name == "kernel_input_transform" and L["plan"].tile_in > 8 else 1
+                order.append({"layer": li, "kernel": name, "launches": a.steps, "dispatches": a.steps * per,
+                              "bytes": work[name]["bytes"], "flops": work[name].get("flops", 0),
+                              "shape": f"{L['hw']}x{L['hw']} {L['C']}->{L['K']}", "moduli": L["spec"].moduli})
+        os.makedirs(os.path.dirname(os.path.abspath(a.order_out)), exist_ok=True)
+        with open(a.order_out, "w") as f:
+            json.dump({"dtype": dtype, "N": N, "order": order}, f)
+        print(json.dumps({"profiled": "each", "groups": len(order), "order": a.order_out}))
+        return 0
+
     if a.profile_kernel:
         li = a.profile_layer
         L = stack.layers[li]
@@ -343,6 +367,117 @@ def run_vgg(a):
     return 0
 
 
+STAGE_TRACE_NAMES = {"kernel_input_transform": ("kernel_input_transform<", "kernel_transform<", "input_transform<"),
+                     "contract": ("contract_stream_kernel<", "contract_kernel<", "contract_pairwise_kernel<"),
+                     "output_transform": ("output_transform<",), "contract_output": ("contract_output_kernel<",),
+                     "kernel_transform": ("kernel_transform<",), "input_contract_output": ("contract_output_kernel<",)}
+
+
+def _read_csv(path):
+    import csv
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _profile_groups(rows, info):
+    """The dispatch rows of each recorded (layer, kernel) group of a
+    ``--profile-kernel each`` run: the last dispatches of the library's
+    kernels in dispatch order, each layer's uncounted first launch of each
+    stage skipped."""
+    warm = {}
+    for g in info["order"]:
+        warm[g["layer"]] = warm.get(g["layer"], 0) + g["dispatches"] // g["launches"]
+    total = sum(g["dispatches"] for g in info["order"]) + sum(warm.values())
+    rows = rows[len(rows) - total:]
+    out, i, seen = [], 0, set()
+    for g in info["order"]:
+        if g["layer"] not in seen:
+            seen.add(g["layer"])
+            i += warm[g["layer"]]
+        grp = rows[i:i + g["dispatches"]]
+        i += g["dispatches"]
+        for r in grp:
+            if not any(n in r["Kernel_Name"] for n in STAGE_TRACE_NAMES[g["kernel"]]):
+                raise SystemExit(f"trace does not follow the recorded order at {g}: {r['Kernel_Name'][:80]}")
+        out.append(grp)
+    return out
+
+
+def summarize_trace(trace_csv, order_json, counters=None):
+    """Markdown table (kernel x layer) of the average dispatch duration from a
+    rocprofv3 kernel trace of ``bench.py --profile-kernel each``; with
+    ``counters`` (FETCH_SIZE and WRITE_SIZE collections of the same mode and
+    of the 256 MiB copy), also each group's HBM bytes per launch (medians,
+    scaled by the copy's true bytes over its readings)."""
+    import statistics
+    with open(order_json) as f:
+        info = json.load(f)
+    ours = lambda rows: [r for r in rows if "wg::" in r["Kernel_Name"]]   # noqa: E731
+    trace = sorted(ours(_read_csv(trace_csv)), key=lambda r: int(r["Start_Timestamp"]))
+    groups = _profile_groups(trace, info)
+    traffic = None
+    if counters:
+        fetch_csv, write_csv, cf_csv, cw_csv = counters[:4]
+        cinfo = info
+        if len(counters) > 4:          # the counter runs' own launch order
+            with open(counters[4]) as f:
+                cinfo = json.load(f)
+        by_id = lambda rows: sorted(ours(rows), key=lambda r: int(r["Dispatch_Id"]))   # noqa: E731
+        fg = _profile_groups(by_id(_read_csv(fetch_csv)), cinfo)
+        wg = _profile_groups(by_id(_read_csv(write_csv)), cinfo)
+        true_bytes = 64 * 1024 * 1024 * 4
+        cf = statistics.median(float(r["Counter_Value"]) for r in _read_csv(cf_csv) if "copyBuffer" in r["Kernel_Name"])
+        cw = statistics.median(float(r["Counter_Value"]) for r in _read_csv(cw_csv) if "copyBuffer" in r["Kernel_Name"])
+        rs, ws = true_bytes / (cf * 1024), true_bytes / (cw * 1024)
+        traffic = [statistics.median(float(r["Counter_Value"]) for r in f) * 1024 * rs
+                   + statistics.median(float(r["Counter_Value"]) for r in w) * 1024 * ws for f, w in zip(fg, wg)]
+    dt = info["dtype"]
+    head = "| layer | shape | kernel | dispatches | average (us) | algorithmic work | rate | fraction of peak |"
+    sep = "|---|---|---|---|---|---|---|---|"
+    if traffic:
+        head += " HBM bytes per launch (counters) | traffic / algorithmic |"
+        sep += "---|---|"
+    lines = [head, sep]
+    tot = 0.0
+    for gi, (g, grp) in enumerate(zip(info["order"], groups)):
+        us = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in grp) / 1e3 / g["launches"]
+        tot += us
+        roof = roofline(g["kernel"], {"bytes": g["bytes"], "flops": g["flops"]}, us, dt)
+        work = f"{g['bytes'] / 1e6:.1f} MB" + (f", {g['flops'] / 1e9:.2f} GFLOP" if g["flops"] else "")
+        line = (f"| {g['layer']} | {g['shape']} | `{g['kernel']}` | {g['dispatches']} | {us:.2f} | {work} | "
+                f"{roof['achieved']} {roof['unit']} | {roof['frac']:.3f} ({roof['bound']}) |")
+        if traffic:
+            line += f" {traffic[gi] / 1e6:.1f} MB | {traffic[gi] / g['bytes']:.2f} |"
+        lines.append(line)
+    lines.append(f"| all | | | | {tot:.2f} (sum over layers and kernels) |" + " |" * (len(sep.split("|")) - 7))
+    return "\n".join(lines)
+
+
+def summarize_counters(kernel, tag, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
+    """HBM bytes per dispatch of one kernel from rocprofv3 FETCH_SIZE and
+    WRITE_SIZE runs (median over its dispatches), scaled by what the same
+    counters read for a plain 256 MiB device copy; a traffic record as JSON."""
+    import statistics
+
+    def med(path, pick):
+        vals = [float(r["Counter_Value"]) for r in _read_csv(path) if pick(r["Kernel_Name"])]
+        return statistics.median(vals), len(vals)
+
+    names = STAGE_TRACE_NAMES[kernel]
+    ours = lambda n: "wg::" in n and any(x in n for x in names)   # noqa: E731
+    copy = lambda n: "copyBuffer" in n                           # noqa: E731
+    fk, nf = med(fetch_csv, ours)
+    wk, nw = med(write_csv, ours)
+    cf, _ = med(copy_fetch_csv, copy)
+    cw, _ = med(copy_write_csv, copy)
+    true_bytes = 64 * 1024 * 1024 * 4
+    rs, ws = true_bytes / (cf * 1024), true_bytes / (cw * 1024)
+    return {"kernel": kernel, "workload": tag, "fetch_kib": fk, "write_kib": wk, "dispatches": [nf, nw],
+            "copy_fetch_kib": cf, "copy_write_kib": cw, "read_scale": rs, "write_scale": ws,
+            "hbm_bytes_per_launch": int(round(fk * 1024 * rs + wk * 1024 * ws)),
+            "source": KERNEL_SOURCES[kernel], "source_sha256_16": source_hash(KERNEL_SOURCES[kernel])}
+
+
 def profile_copy(a, dev):
     """A plain 256 MiB device copy, --steps times: the calibration of the
     byte counters (its true traffic is known)."""
@@ -380,11 +515,31 @@ def main(argv=None):
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="CPU oracle time budget (0 disables the cpu_baseline leg)")
     ap.add_argument("--graph", action="store_true", help="replay each step from a captured HIP graph")
-    ap.add_argument("--profile-kernel", default=None, choices=KERNEL_NAMES + ("copy",),
+    ap.add_argument("--profile-kernel", default=None, choices=KERNEL_NAMES + ("copy", "each"),
                     help="only launch this kernel, --steps times (for counter collection); 'copy' "
-                         "launches a plain 256 MiB device copy to calibrate the byte counters")
+                         "launches a plain 256 MiB device copy to calibrate the byte counters; 'each' "
+                         "launches every stage kernel of every VGG layer in turn (for a kernel trace)")
     ap.add_argument("--profile-layer", type=int, default=1, help="VGG layer of --profile-kernel (0..12)")
+    ap.add_argument("--order-out", default="gpurun_out/vgg_profile_order.json",
+                    help="where --profile-kernel each records its launch order")
+    ap.add_argument("--summarize-trace", nargs="+", default=None,
+                    metavar="TRACE_CSV ORDER_JSON [FETCH_CSV WRITE_CSV COPY_FETCH_CSV COPY_WRITE_CSV [ORDER_JSON]]",
+                    help="print the kernel x layer table of a kernel trace of --profile-kernel each, with HBM "
+                         "bytes from counter runs of the same mode if given (no GPU)")
+    ap.add_argument("--summarize-counters", nargs=4, default=None,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="print the traffic record of --profile-kernel from counter runs (no GPU)")
+    ap.add_argument("--traffic-tag", default="vgg16_bf16_l1", help="workload tag of --summarize-counters")
     a = ap.parse_args(argv)
+
+    if a.summarize_trace:
+        if len(a.summarize_trace) not in (2, 6, 7):
+            ap.error("--summarize-trace takes 2, 6 or 7 files")
+        print(summarize_trace(a.summarize_trace[0], a.summarize_trace[1], a.summarize_trace[2:] or None))
+        return 0
+    if a.summarize_counters:
+        print(json.dumps(summarize_counters(a.profile_kernel, a.traffic_tag, *a.summarize_counters), indent=1))
+        return 0
 
     if a.gpus != 1:
         print(f"bench.py: this library runs on one GPU; --gpus {a.gpus} is not supported "

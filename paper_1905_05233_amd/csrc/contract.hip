@@ -70,7 +70,15 @@ __global__ __launch_bounds__(kThreads, 2) void contract_kernel(const unsigned ch
                                                               int num_nb) {
     __shared__ u32x4 lds[2][(kBM + kBN) * kLdsChunks];
 
-    int bid = blockIdx.x;
+    // XCD-aware numbering: the hardware deals workgroup ids round-robin over
+    // the 8 XCDs, each with its own L2; giving each XCD a contiguous run of
+    // blocks keeps the column blocks of one row block (same V rows) and the
+    // row blocks of one domain point (same U plane) in one L2, instead of V
+    // being fetched from HBM once per XCD that needs it
+    const int64_t G = gridDim.x;
+    const int64_t b0 = blockIdx.x;
+    const int64_t xcd = b0 % 8;
+    int bid = static_cast<int>(xcd * (G / 8) + std::min<int64_t>(xcd, G % 8) + b0 / 8);
     const int nb = bid % num_nb;
     bid /= num_nb;
     const int mb = bid % num_mb;
