@@ -189,12 +189,27 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
         const int row = r8 + (lane >> 3);
         roff[j] = static_cast<uint32_t>((row < krows ? row : row - krows) * rb + piece);
     }
+    // wide: the block's rows in plane 0, the plane strides and the
+    // loop-invariant record counts of the buffer descriptors (rows past K or T
+    // of a plane read zero), so that a request only multiplies its small plane
+    // index by a stride
+    const unsigned char* bu = U + k0 * rb;
+    const unsigned char* bv = V + t0 * rb;
+    const uint64_t plane_u = static_cast<uint64_t>(K * rb), plane_v = static_cast<uint64_t>(T * rb);
+    const int64_t rec_u64 = (K - k0) * rb, rec_v64 = (T - t0) * rb;
+    const int rec_u = static_cast<int>(static_cast<uint32_t>(rec_u64 > 0xffffffffLL ? 0xffffffffLL : rec_u64));
+    const int rec_v = static_cast<int>(static_cast<uint32_t>(rec_v64 > 0xffffffffLL ? 0xffffffffLL : rec_v64));
     // wide: the request is (xi, slice); narrow: the step's first domain point
     // in visiting order (a fastest), each lane's plane found from its lxi
     auto issue = [&](unsigned char* st, int xi, int sl, int q0, bool any) __attribute__((always_inline)) {
         if constexpr (!NARROW) {
-            const auto ru = make_rsrc(U + (static_cast<int64_t>(xi) * K + k0) * rb, (K - k0) * rb);
-            const auto rv = make_rsrc(V + (static_cast<int64_t>(xi) * T + t0) * rb, (T - t0) * rb);
+            const uint64_t ux = static_cast<uint32_t>(xi);   // 0 <= xi < alpha'^2
+            const auto ru = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(bu + ux * plane_u),
+                                                              static_cast<short>(0), rec_u,
+                                                              static_cast<int>(kRsrcWord3));
+            const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(bv + ux * plane_v),
+                                                              static_cast<short>(0), rec_v,
+                                                              static_cast<int>(kRsrcWord3));
             const int sb = sl * kSlice;
             const bool in = any && sb + piece < rb;   // zero past the row
 #pragma unroll
