@@ -277,11 +277,11 @@ hipError_t launch_ot(int dt, const wg::Geometry& g, const wg::OutputTable& t, co
     }
 }
 hipError_t launch_co(int dt, const wg::Geometry& g, const wg::OutputTable& t, const void* V, const void* U,
-                     void* y, hipStream_t s) {
+                     void* y, int bi, hipStream_t s) {
     switch (dt) {
-        case 0: return wg::launch_contract_output_t<0>(g, t, V, U, y, s);
-        case 1: return wg::launch_contract_output_t<1>(g, t, V, U, y, s);
-        default: return wg::launch_contract_output_t<2>(g, t, V, U, y, s);
+        case 0: return wg::launch_contract_output_t<0>(g, t, V, U, y, bi, s);
+        case 1: return wg::launch_contract_output_t<1>(g, t, V, U, y, bi, s);
+        default: return wg::launch_contract_output_t<2>(g, t, V, U, y, bi, s);
     }
 }
 hipError_t launch_ico(int dt, const wg::Geometry& g, const wg::InputTable& it, const wg::OutputTable& ot,
@@ -512,7 +512,7 @@ wg_status conv2d_with(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_t
                  "kernel and input transforms");
     if (s != WG_OK) return s;
     if (L.path == WG_PATH_FUSED)
-        return from_hip(launch_co(dt, L.g, plan->otab, V, U, y->data, stream), "fused contraction");
+        return from_hip(launch_co(dt, L.g, plan->otab, V, U, y->data, plan->builtin, stream), "fused contraction");
     if ((s = from_hip(launch_ct(dt, L.g, V, U, M, stream, plan->channel_sum), "contraction")) != WG_OK) return s;
     return from_hip(launch_ot(dt, L.g, plan->otab, M, y->data, plan->builtin, stream), "output transform");
 }
@@ -671,7 +671,7 @@ wg_status winograd_contract_output(wg_plan plan, const void* V, const void* U, i
     const wg::Geometry g = wg::make_geometry(y->n, y->h, y->w, C, y->c, plan->tr.m, plan->tr.alpha);
     if (!fused_supported(plan->dtype, g))
         return fail(WG_ERR_UNSUPPORTED, "the fused kernel does not support this layer shape");
-    return from_hip(launch_co(plan->dtype, g, plan->otab, V, U, y->data, stream), "fused contraction");
+    return from_hip(launch_co(plan->dtype, g, plan->otab, V, U, y->data, plan->builtin, stream), "fused contraction");
 }
 
 wg_status winograd_input_contract_output(wg_plan plan, const wg_tensor* x, const void* U, wg_tensor* y,

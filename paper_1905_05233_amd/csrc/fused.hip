@@ -26,7 +26,10 @@
 // read as zero.
 #include <algorithm>
 #include <cstring>
+#include <type_traits>
+#include <utility>
 
+#include "coefs.hpp"
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -535,6 +538,330 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Whole channel rows per step, with the domain-point loop unrolled.
+//
+// When a channel row fits NSL 128-byte slices (NSL = 1: C <= 64 in fp16/bf16,
+// C <= 32 in fp32; NSL = 2: twice that) and the block is 64 output channels x
+// 32 tiles (WT = 2), the contraction of a domain point is a single step of NSL
+// slices, and this variant unrolls the alpha'^2 steps at compile time: the
+// output-transform coefficients of every fold are constants (for a built-in
+// plan the zero terms disappear; for any other plan they are read from the
+// kernel arguments once), and no step bookkeeping is left.  Each step's U and
+// V rows are staged in LDS by buffer-to-LDS loads in the layout of the looped
+// kernel (rows of 128 bytes per slice, XOR-swizzled 16-byte pieces), NST
+// stages deep; each wave loads whole rows with 8 lanes per row, so its
+// requests are coalesced.  The output tile leaves through LDS: each wave
+// parks its channels of every pixel there, and the block's pixels are then
+// written with 16 contiguous bytes per lane (whole 64-channel runs of each
+// pixel) instead of 4 channels per lane.  Folds, rounding and the order of
+// every sum are those of the looped kernel.
+
+// f(std::integral_constant<int, S>) for S = 0 .. N-1, in order
+template <class F, int... S>
+__device__ __forceinline__ void unroll_seq(F& f, std::integer_sequence<int, S...>) {
+    (f(std::integral_constant<int, S>{}), ...);
+}
+template <int N, class F> __device__ __forceinline__ void unroll(F&& f) {
+    unroll_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+// Stages of the unrolled kernel and LDS bytes of one stage (NSL slices of 96
+// rows: 64 channel rows, then 32 tile rows)
+template <int NSL> constexpr int unrolled_stages() { return NSL == 1 ? 4 : 3; }
+template <int NSL> constexpr int unrolled_stage_bytes() { return NSL * kStageBytes; }
+// LDS of the output tile in the epilogue: 16 tiles x m^2 pixels x 64 channels
+template <int MM, class Elem> constexpr int unrolled_out_bytes() {
+    return 16 * MM * MM * 64 * static_cast<int>(sizeof(Elem));
+}
+
+// Vector-memory groups (one per step) a wave has issued after that of step s
+// when step s begins: the prologue requests steps 0 .. NST-2, and step s'
+// requests step s' + NST - 1.
+template <int NSTEPS, int NST>
+constexpr int groups_after(int s) {
+    const int issued = (s + NST - 1 < NSTEPS) ? s + NST - 1 : NSTEPS;
+    return issued - (s + 1);
+}
+
+template <int D, int MM, int ALPHA, class CO, int NSL>
+__global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
+    const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, typename DTypeOf<D>::type* __restrict__ y,
+    OutputTable tab, Geometry geo, int n_kb, int rb) {
+    using Elem = typename DTypeOf<D>::type;
+    using S = Storage<Elem>;
+    constexpr int WT = 2;                  // two 16-tile blocks per wave
+    constexpr int NSTEPS = ALPHA * ALPHA;
+    constexpr int NST = unrolled_stages<NSL>();
+    constexpr int kSB = unrolled_stage_bytes<NSL>();
+    constexpr int kKD = 3 * NSL;           // DMA instructions per wave and step
+    constexpr int kOut = unrolled_out_bytes<MM, Elem>();
+    constexpr int kLds = NST * kSB > kOut ? NST * kSB : kOut;
+    static_assert(kKD * (NST - 2) < 64, "vmcnt holds 6 bits");
+    static_assert(2 * kLds <= 160 * 1024, "two workgroups per CU");
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[kLds];
+
+    // XCD-aware numbering, as in contract_output_kernel
+    const int64_t G = gridDim.x;
+    const int64_t bid = blockIdx.x;
+    const int64_t xcd = bid % 8;
+    const int64_t unit = xcd * (G / 8) + std::min<int64_t>(xcd, G % 8) + bid / 8;
+    const int kb = static_cast<int>(unit % n_kb);
+    const int64_t tb = unit / n_kb;
+    const int64_t k0 = static_cast<int64_t>(kb) * 64;
+    const int64_t t0 = tb * 32;
+    const int64_t T = geo.T, K = geo.K;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // 16 output channels each
+    const int grp = lane >> 4;
+    const int l16 = lane & 15;
+
+    // DMA map (the looped kernel's): instruction j of wave w fills stage rows
+    // 8 (w + 4 j) .. + 7 of each slice, channel rows 0 .. 63 first, then tile
+    // rows; lane l lands at row 8 (w + 4 j) + l / 8, 16-byte column l % 8, and
+    // fetches piece (l % 8) ^ (l / 8) of its row; pieces past the row read zero
+    const int lp = (lane & 7) ^ (lane >> 3);
+    uint32_t roff[3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+        const int row = 8 * (wave + 4 * j) + (lane >> 3);
+        roff[j] = static_cast<uint32_t>((row < 64 ? row : row - 64) * rb + lp * 16);
+    }
+    // descriptors over one plane's rows of the block (rows past K or T read zero)
+    const unsigned char* bu = U + k0 * rb;
+    const unsigned char* bv = V + t0 * rb;
+    const uint64_t plane_u = static_cast<uint64_t>(K * rb), plane_v = static_cast<uint64_t>(T * rb);
+    const int64_t rec_u64 = (K - k0) * rb, rec_v64 = (T - t0) * rb;
+    const int rec_u = static_cast<int>(static_cast<uint32_t>(rec_u64 > 0xffffffffLL ? 0xffffffffLL : rec_u64));
+    const int rec_v = static_cast<int>(static_cast<uint32_t>(rec_v64 > 0xffffffffLL ? 0xffffffffLL : rec_v64));
+
+    // step s is the domain point (a, b) = (s % alpha', s / alpha'), xi = a alpha' + b
+    auto issue = [&](auto sc) __attribute__((always_inline)) {
+        constexpr int s = decltype(sc)::value;
+        constexpr uint64_t xi = (s % ALPHA) * ALPHA + s / ALPHA;
+        const auto ru = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(bu + xi * plane_u),
+                                                          static_cast<short>(0), rec_u, static_cast<int>(kRsrcWord3));
+        const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(bv + xi * plane_v),
+                                                          static_cast<short>(0), rec_v, static_cast<int>(kRsrcWord3));
+        unsigned char* st = lds + (s % NST) * kSB;
+#pragma unroll
+        for (int sl = 0; sl < NSL; ++sl) {
+            const bool in = sl * kSlice + lp * 16 < rb;
+#pragma unroll
+            for (int j = 0; j < 3; ++j)
+                dma16(j < 2 ? ru : rv, st + sl * kStageBytes + (wave + 4 * j) * 1024,
+                      in ? roff[j] + sl * kSlice : kOob);
+        }
+    };
+
+    f32x4 part[WT];
+    float Z[WT][MM][4];
+    float Y[WT][MM][MM][4];
+#pragma unroll
+    for (int w = 0; w < WT; ++w)
+#pragma unroll
+        for (int o = 0; o < MM; ++o)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                Z[w][o][r] = 0.0f;
+#pragma unroll
+                for (int q = 0; q < MM; ++q) Y[w][o][q][r] = 0.0f;
+            }
+
+    // M of step s (in part) into Z, and Z into the output tile after a column
+    auto fold = [&](auto sc) __attribute__((always_inline)) {
+        constexpr int s = decltype(sc)::value;
+        constexpr int a = s % ALPHA, bc = s / ALPHA;
+#pragma unroll
+        for (int o = 0; o < MM; ++o) {
+            const float c = CO::at(tab, o * ALPHA + a);
+#pragma unroll
+            for (int w = 0; w < WT; ++w)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) Z[w][o][r] = term<CO>(c, part[w][r], Z[w][o][r]);
+        }
+        if constexpr (a == ALPHA - 1) {
+#pragma unroll
+            for (int q = 0; q < MM; ++q) {
+                const float c = CO::at(tab, q * ALPHA + bc);
+#pragma unroll
+                for (int w = 0; w < WT; ++w)
+#pragma unroll
+                    for (int o = 0; o < MM; ++o)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) Y[w][o][q][r] = term<CO>(c, Z[w][o][r], Y[w][o][q][r]);
+            }
+#pragma unroll
+            for (int w = 0; w < WT; ++w)
+#pragma unroll
+                for (int o = 0; o < MM; ++o)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) Z[w][o][r] = 0.0f;
+        }
+    };
+
+    // fragments: A = channel row 16 wave + l16, B = tile row 16 w + l16 of
+    // each slice, pieces grp and grp + 4 (row & 7 = l16 & 7 for both)
+    const int swz = l16 & 7;
+    const int a_row = (wave * 16 + l16) * kSlice;
+    const int b_row = (64 + l16) * kSlice;
+    const int col0 = (grp ^ swz) * 16;
+    const int col1 = ((grp + 4) ^ swz) * 16;
+    auto step = [&](auto sc) __attribute__((always_inline)) {
+        constexpr int s = decltype(sc)::value;
+        // each step is scheduled on its own (else the scheduler interleaves the
+        // straight-line steps and runs out of registers)
+        __builtin_amdgcn_sched_barrier(0);
+        // this wave's requests of step s have landed once at most the later
+        // groups are outstanding; the barrier makes every wave's visible and
+        // frees the stage read in the previous step for the next request
+        __builtin_amdgcn_s_waitcnt(vm_wait(kKD * groups_after<NSTEPS, NST>(s)));
+        lds_barrier();
+        if constexpr (s + NST - 1 < NSTEPS) issue(std::integral_constant<int, s + NST - 1>{});
+        const unsigned char* cur = lds + (s % NST) * kSB;
+        u32x4 fa0 = lds_read16(cur + a_row + col0);
+        u32x4 fa1 = lds_read16(cur + a_row + col1);
+        u32x4 fb00 = lds_read16(cur + b_row + col0);
+        u32x4 fb01 = lds_read16(cur + b_row + col1);
+        u32x4 fb10 = lds_read16(cur + b_row + 16 * kSlice + col0);
+        u32x4 fb11 = lds_read16(cur + b_row + 16 * kSlice + col1);
+        if constexpr (s > 0) fold(std::integral_constant<int, s - 1>{});
+        lds_settle(fa0, fa1, fb00, fb01, fb10, fb11);
+        part[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        part[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        mma<D>(fa0, fb00, part[0]);
+        mma<D>(fa0, fb10, part[1]);
+        mma<D>(fa1, fb01, part[0]);
+        mma<D>(fa1, fb11, part[1]);
+        if constexpr (NSL == 2) {
+            // the second slice, its fragments read after the first slice's
+            // MFMAs have taken theirs (the register sets are reused)
+            cur += kStageBytes;
+            fa0 = lds_read16(cur + a_row + col0);
+            fa1 = lds_read16(cur + a_row + col1);
+            fb00 = lds_read16(cur + b_row + col0);
+            fb01 = lds_read16(cur + b_row + col1);
+            fb10 = lds_read16(cur + b_row + 16 * kSlice + col0);
+            fb11 = lds_read16(cur + b_row + 16 * kSlice + col1);
+            lds_settle(fa0, fa1, fb00, fb01, fb10, fb11);
+            mma<D>(fa0, fb00, part[0]);
+            mma<D>(fa0, fb10, part[1]);
+            mma<D>(fa1, fb01, part[0]);
+            mma<D>(fa1, fb11, part[1]);
+        }
+    };
+
+    // prologue: steps 0 .. NST-2 requested
+    unroll<NST - 1>([&](auto sc) __attribute__((always_inline)) {
+        if constexpr (decltype(sc)::value < NSTEPS) issue(sc);
+    });
+    unroll<NSTEPS>(step);
+    fold(std::integral_constant<int, NSTEPS - 1>{});
+    // the output tile is complete here: without this, the compiler sinks the
+    // folds of every step into the (conditional) store code after the loop
+#pragma unroll
+    for (int w = 0; w < WT; ++w)
+#pragma unroll
+        for (int o = 0; o < MM; ++o)
+#pragma unroll
+            for (int q = 0; q < MM; ++q)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) asm volatile("" : "+v"(Y[w][o][q][r]));
+
+    // epilogue, one 16-tile block at a time: each lane parks its four
+    // channels of every pixel in LDS (records of 64 channels per pixel, the
+    // 16-byte chunks XOR-swizzled by tile), then the block's records go out
+    // with 16 contiguous bytes per lane.  Channel counts that are not a
+    // multiple of a 16-byte chunk take the direct per-lane store instead.
+    constexpr int ES = static_cast<int>(sizeof(Elem));
+    constexpr int kRec = 64 * ES;               // bytes of a pixel record
+    constexpr int kPx = MM * MM;                // pixels of a tile
+    constexpr int kLanesPerRec = kRec / 16;
+    constexpr int kRecPerIns = 64 / kLanesPerRec;
+    constexpr int kInsPerWave = 16 * kPx / kRecPerIns / 4;
+    const bool staged = (K * ES) % 16 == 0;
+    if (staged) {
+        unsigned char* ybytes = reinterpret_cast<unsigned char*>(y);
+        const int chunk = lane % kLanesPerRec;
+        // coordinates of the block's first tile; a later tile of the block is
+        // reached by stepping (T < 2^31 here, so 32-bit arithmetic)
+        const int tw = static_cast<int>(geo.tw), th = static_cast<int>(geo.th);
+        const int H = static_cast<int>(geo.H), W = static_cast<int>(geo.W);
+        const int tx0 = static_cast<int>(t0 % geo.tw);
+        const int ty0 = static_cast<int>((t0 / geo.tw) % geo.th);
+        const int n0 = static_cast<int>(t0 / (geo.tw * geo.th));
+#pragma unroll
+        for (int w = 0; w < WT; ++w) {
+            // every wave is done with the LDS (the stages, or the previous block's records)
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            lds_barrier();
+#pragma unroll
+            for (int o = 0; o < MM; ++o)
+#pragma unroll
+                for (int q = 0; q < MM; ++q) {
+                    const int rec = l16 * kPx + o * MM + q;
+                    const int byte = (wave * 16 + 4 * grp) * ES;      // within the record
+                    const int phys = (((byte >> 4) ^ (l16 & 7)) << 4) | (byte & 15);
+                    unsigned char* dst = lds + rec * kRec + phys;
+                    if constexpr (ES == 4) {
+                        *reinterpret_cast<f32x4*>(dst) = f32x4{Y[w][o][q][0], Y[w][o][q][1], Y[w][o][q][2], Y[w][o][q][3]};
+                    } else {
+                        const uint32_t lo = bits16(S::from_f32(Y[w][o][q][0])) | (bits16(S::from_f32(Y[w][o][q][1])) << 16);
+                        const uint32_t hi = bits16(S::from_f32(Y[w][o][q][2])) | (bits16(S::from_f32(Y[w][o][q][3])) << 16);
+                        *reinterpret_cast<u32x2*>(dst) = u32x2{lo, hi};
+                    }
+                }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the records are in LDS
+            lds_barrier();
+#pragma unroll
+            for (int i = 0; i < kInsPerWave; ++i) {
+                const int rec = (wave * kInsPerWave + i) * kRecPerIns + lane / kLanesPerRec;
+                const int tl = rec / kPx, px = rec % kPx;
+                const u32x4 v = *reinterpret_cast<const u32x4*>(lds + rec * kRec + ((chunk ^ (tl & 7)) << 4));
+                int tx = tx0 + w * 16 + tl, ty = ty0, n = n0;
+                while (tx >= tw) {
+                    tx -= tw;
+                    if (++ty == th) {
+                        ty = 0;
+                        ++n;
+                    }
+                }
+                const int hr = ty * MM + px / MM, wc = tx * MM + px % MM;
+                const int64_t ch = k0 + chunk * (16 / ES);
+                if (t0 + w * 16 + tl < T && hr < H && wc < W && ch < K)
+                    *reinterpret_cast<u32x4*>(ybytes + ((static_cast<int64_t>(n * H + hr) * W + wc) * K + ch) * ES) = v;
+            }
+        }
+        return;
+    }
+    const int64_t k = k0 + wave * 16 + 4 * grp;
+    if (k >= K) return;
+#pragma unroll
+    for (int w = 0; w < WT; ++w) {
+        const int64_t tile = t0 + w * 16 + l16;
+        if (tile >= T) continue;
+        const int64_t tx = tile % geo.tw;
+        const int64_t ty = (tile / geo.tw) % geo.th;
+        const int64_t n = tile / (geo.tw * geo.th);
+#pragma unroll
+        for (int o = 0; o < MM; ++o) {
+            const int64_t hr = ty * MM + o;
+            if (hr >= geo.H) break;
+#pragma unroll
+            for (int q = 0; q < MM; ++q) {
+                const int64_t wc = tx * MM + q;
+                if (wc >= geo.W) break;
+                Elem* dst = y + ((n * geo.H + hr) * geo.W + wc) * K + k;
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (k + r < K) dst[r] = S::from_f32(Y[w][o][q][r]);
+            }
+        }
+    }
+}
+
 // tile blocks per wave: as many as the output-tile registers allow (Y holds
 // m^2 values per channel-tile pair), fewer when that leaves CUs idle
 int pick_wt(const Geometry& g, int kw) {
@@ -594,10 +921,23 @@ hipError_t launch_co_instance(const CoArgs& c, hipStream_t stream) {
     }
 }
 
-// x == nullptr: V from memory; else the input transform in the prologue
+template <int D, int TT, int A, class CO>
+hipError_t launch_unrolled_instance(const CoArgs& c, hipStream_t stream) {
+    using Elem = typename DTypeOf<D>::type;
+    if (c.n_slices == 1)
+        hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, 1>), dim3(c.nb), dim3(kThreads), 0,
+                           stream, c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.n_kb, c.rb);
+    else
+        hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, 2>), dim3(c.nb), dim3(kThreads), 0,
+                           stream, c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.n_kb, c.rb);
+    return hipGetLastError();
+}
+
+// x == nullptr: V from memory; else the input transform in the prologue.
+// builtin: id of the built-in plan with the same tables, or -1.
 template <int D>
 hipError_t launch_co(const Geometry& g, const OutputTable& tab, const void* V, const void* U, void* y,
-                     const void* x, const InputTable* itab, hipStream_t stream) {
+                     const void* x, const InputTable* itab, int builtin, hipStream_t stream) {
     const int rb = static_cast<int>(g.Cp * (D == 0 ? 4 : 2));
     const int kw0 = g.K <= 16 ? 1 : g.K <= 32 ? 2 : 4;
     const int wt = pick_wt(g, std::max(kw0, 2));
@@ -628,6 +968,25 @@ hipError_t launch_co(const Geometry& g, const OutputTable& tab, const void* V, c
     if (itab) c.itab = *itab;
     else std::memset(&c.itab, 0, sizeof(c.itab));
     c.nb = static_cast<unsigned>(grid);
+    if (!x && xp == 1 && c.n_slices <= 2 && wt == 2 && kw == 4) {
+        // one step per domain point, blocks of 64 output channels x 32 tiles
+        switch (builtin) {
+#define WG_UNR_BUILTIN(ID, TT, A)                                                                          \
+    case ID:                                                                                               \
+        if constexpr (TT <= 6)                                                                             \
+            if (g.t == TT && g.alpha == A) return launch_unrolled_instance<D, TT, A, ConstCoefs<BuiltinPlan##ID>>(c, stream); \
+        break;
+            WG_BUILTIN_PLANS(WG_UNR_BUILTIN)
+#undef WG_UNR_BUILTIN
+            default:
+                break;
+        }
+#define WG_UNR_CASE(TT, A) \
+        if (g.t == TT && g.alpha == A) return launch_unrolled_instance<D, TT, A, RuntimeCoefs>(c, stream);
+        WG_UNR_CASE(4, 4) WG_UNR_CASE(4, 5) WG_UNR_CASE(4, 6) WG_UNR_CASE(4, 7)
+        WG_UNR_CASE(6, 6) WG_UNR_CASE(6, 7) WG_UNR_CASE(6, 8) WG_UNR_CASE(6, 9)
+#undef WG_UNR_CASE
+    }
 #define WG_CO_CASE(TT, A, W)                                                                              \
     if (g.t == TT && g.alpha == A && wt == W) {                                                           \
         if (x && xp == 8) return launch_co_instance<D, TT, A, W, true, 8, true>(c, stream);               \
@@ -649,9 +1008,9 @@ hipError_t launch_co(const Geometry& g, const OutputTable& tab, const void* V, c
 
 template <>
 hipError_t launch_contract_output_t<WG_DTYPE>(const Geometry& g, const OutputTable& tab, const void* V,
-                                              const void* U, void* y, hipStream_t stream) {
+                                              const void* U, void* y, int builtin, hipStream_t stream) {
     if (!contract_output_supported_t<WG_DTYPE>(g)) return hipErrorInvalidValue;
-    return launch_co<WG_DTYPE>(g, tab, V, U, y, nullptr, nullptr, stream);
+    return launch_co<WG_DTYPE>(g, tab, V, U, y, nullptr, nullptr, builtin, stream);
 }
 
 template <>
@@ -659,7 +1018,7 @@ hipError_t launch_input_contract_output_t<WG_DTYPE>(const Geometry& g, const Inp
                                                     const OutputTable& otab, const void* x, const void* U, void* y,
                                                     hipStream_t stream) {
     if (!input_contract_output_supported_t<WG_DTYPE>(g) || !x) return hipErrorInvalidValue;
-    return launch_co<WG_DTYPE>(g, otab, nullptr, U, y, x, &itab, stream);
+    return launch_co<WG_DTYPE>(g, otab, nullptr, U, y, x, &itab, -1, stream);
 }
 
 }  // namespace wg

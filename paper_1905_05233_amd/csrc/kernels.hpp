@@ -110,7 +110,7 @@ hipError_t launch_contract_pairwise_t(const Geometry& g, const void* V, const vo
 template <int D> bool contract_output_supported_t(const Geometry& g);
 template <int D>
 hipError_t launch_contract_output_t(const Geometry& g, const OutputTable& tab, const void* V, const void* U,
-                                    void* y, hipStream_t stream);
+                                    void* y, int builtin, hipStream_t stream);
 // The same kernel with the input transform in its prologue: x, U -> y, no V
 // in memory.  Supported for channel rows of at most 32 bytes and K > 32.
 template <int D> bool input_contract_output_supported_t(const Geometry& g);

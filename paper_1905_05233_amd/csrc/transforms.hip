@@ -19,7 +19,7 @@
 // register arrays have compile-time sizes.
 #include <utility>
 
-#include "builtin_plans.hpp"
+#include "coefs.hpp"
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -32,27 +32,6 @@ namespace wg {
 namespace {
 
 constexpr int kBlock = 256;
-
-// Transform coefficients of the input and output transforms: read from the
-// kernel-argument tables (any plan) or, for the built-in plans, compile-time
-// constants, with which the compiler drops every term whose coefficient is
-// zero.  Dropping a zero term leaves the sum unchanged for finite data (up to
-// the sign of a zero result).
-struct RuntimeCoefs {
-    static constexpr bool kConst = false;
-    static __device__ __forceinline__ float bt(const InputTable& t, int i) { return t.bt[i]; }
-    static __device__ __forceinline__ float at(const OutputTable& t, int i) { return t.at[i]; }
-};
-template <class P> struct ConstCoefs {
-    static constexpr bool kConst = true;
-    static __device__ __forceinline__ constexpr float bt(const InputTable&, int i) { return P::bt[i]; }
-    static __device__ __forceinline__ constexpr float at(const OutputTable&, int i) { return P::at[i]; }
-};
-// acc + c * x as one fused multiply-add; skipped for a compile-time zero c
-template <class CO> __device__ __forceinline__ float term(float c, float x, float acc) {
-    if (CO::kConst && c == 0.0f) return acc;
-    return __builtin_fmaf(c, x, acc);
-}
 
 // ----------------------------------------------------------------- kernel
 // U[xi = a*alpha + b][k][c] = sum_j (sum_i G[a][i] g[i][j]) G[b][j]; one thread

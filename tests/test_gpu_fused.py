@@ -119,6 +119,124 @@ def test_fused_matches_separate_vgg_layers(hw, C, K, dtype):
     _fused_vs_separate(WL.F4_A2P1, 4, dtype, (1, hw, hw, C, K), hw + C, f"VGG {hw}x{hw} {C}->{K} {dtype}")
 
 
+# The unrolled fused kernel: channel rows of 65 .. 256 bytes (one or two
+# 128-byte slices per step), m <= 4, more than 32 output channels and enough
+# blocks of 64 channels x 32 tiles to give every CU two (the launcher's rule).
+# One plan per compiled instance: built-in plans (constant coefficients) and
+# plans with run-time coefficients.
+UNROLLED_PLANS = [
+    (WL.F2_LINEAR, 2, False),              # t 4, alpha' 4, built-in
+    (WL.F2_LINEAR, 2, True),               # the same shape, run-time coefficients
+    ("0,a^2+1,inf", 2, False),             # t 4, alpha' 5
+    ("a^2+1,a^2-2", 2, False),             # t 4, alpha' 6
+    (WL.F4_LINEAR, 4, False),              # t 6, alpha' 6, built-in
+    (WL.F4_A2P1, 4, False),                # t 6, alpha' 7, built-in
+    (WL.F4_A2P1, 4, True),                 # the same shape, run-time coefficients
+    ("0,a^2+1,a^2-2,inf", 4, False),       # t 6, alpha' 8
+    ("a^2+1,a^2-2,a^2+2", 4, False),       # t 6, alpha' 9
+]
+
+
+def _unrolled_shape(m, dtype, ragged_k, slices=1):
+    """A layer the launcher sends to the unrolled kernel: rows that leave the
+    last pieces of a 128-byte slice empty, or fill it; ragged tiles; with
+    ``ragged_k`` an output-channel count whose rows end mid 16-byte chunk (the
+    epilogue's direct stores) and a partial block of 64 channels."""
+    if slices == 1:
+        C = {"f32": 20, "f16": 48, "bf16": 64}[dtype]
+    else:
+        C = {"f32": 48, "f16": 100, "bf16": 128}[dtype]
+    K = 250 if ragged_k else 256
+    hw = 254 if m == 4 else 129
+    return 1, hw, hw, C, K
+
+
+def _selects_unrolled(m, C, K, T, dtype):
+    rb = -(-C // 8) * 8 * (4 if dtype == "f32" else 2)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    return m <= 4 and 64 < rb <= 256 and K > 32 and (-(-K // 64)) * (-(-T // 32)) >= 2 * cus
+
+
+def _gpu_stages(p, V, U, M, C, K, N, H, W):
+    """The library's own U, V and M in the oracle's stage layout."""
+    al, m = p.alpha, p.m
+    th, tw = -(-H // m), -(-W // m)
+    return {"V": to_np(V)[:, :, :C].reshape(al, al, N, th, tw, C),
+            "U": to_np(U)[:, :, :C].reshape(al, al, K, C),
+            "M": to_np(M)[:, :, :K].reshape(al, al, N, th, tw, K)}
+
+
+def _unrolled_vs_separate(spec, m, generic, dtype, slices):
+    from paper_1905_05233_amd.winograd import Plan
+    N, H, W, C, K = _unrolled_shape(m, dtype, ragged_k=generic, slices=slices)
+    print(f"[unrolled] {spec} m={m} generic={generic} {dtype} {(N, H, W, C, K)}", flush=True)
+    x, w = _inputs((N, H, W, C, K), dtype, seed=5 * m + C)
+    p = Plan(spec, m=m, dtype=dtype, path="fused", generic_transforms=generic)
+    assert (p.builtin >= 0) == (not generic and spec in (WL.F2_LINEAR, WL.F4_LINEAR, WL.F4_A2P1))
+    g = p.geometry(N, H, W, C, K)
+    assert _selects_unrolled(m, C, K, g["T"], dtype)
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
+    U, V = p.kernel_input_transform(wd, xd)
+    yf = p.contract_output(V, U, C, N, H, W)
+    M = p.contract(V, U, C)
+    ys = p.output_transform(M, N, H, W, K)
+    y_conv = p.conv2d(xd, wd)
+    torch.cuda.synchronize()
+    assert torch.equal(y_conv, yf)
+    st = _gpu_stages(p, V, U, M, C, K, N, H, W)
+    yf64, ys64 = to_np(yf).astype(np.float64), to_np(ys).astype(np.float64)
+    op = OP.build_plan(spec, n_o=m)
+    b = pair_bound(st, op, dtype, yf64, H, W, y_ref=ys64)
+    diff = np.abs(yf64 - ys64)
+    print(f"[unrolled] max |diff| {np.max(diff):.3e}, max diff/bound {np.max(diff / b):.3g}, "
+          f"median bound/|y| {np.median(b / np.maximum(np.abs(ys64), 1e-30)):.3g}", flush=True)
+    assert np.all(np.isfinite(yf64))
+    assert np.all(diff <= b)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("spec,m,generic", UNROLLED_PLANS,
+                         ids=[f"{s}-m{m}" + ("-runtime" if g else "") for s, m, g in UNROLLED_PLANS])
+def test_unrolled_matches_separate(spec, m, generic, dtype):
+    """Fused (unrolled instance, one slice per step) against the separate path
+    on the same U and V, element by element within the bound between two
+    evaluations that differ only in the order of the fp32 channel sums
+    (``pair_bound`` with the separate path as the reference)."""
+    _unrolled_vs_separate(spec, m, generic, dtype, slices=1)
+
+
+UNROLLED_TWO_SLICES = [(WL.F2_LINEAR, 2, False), (WL.F4_A2P1, 4, False), (WL.F4_A2P1, 4, True),
+                       ("0,a^2+1,a^2-2,inf", 4, False)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("spec,m,generic", UNROLLED_TWO_SLICES,
+                         ids=[f"{s}-m{m}" + ("-runtime" if g else "") for s, m, g in UNROLLED_TWO_SLICES])
+def test_unrolled_two_slices_matches_separate(spec, m, generic, dtype):
+    """The same with channel rows of two slices (a step contracts both)."""
+    _unrolled_vs_separate(spec, m, generic, dtype, slices=2)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("spec,m", [(WL.F2_LINEAR, 2), (WL.F4_A2P1, 4)])
+def test_unrolled_builtin_equals_runtime_coefficients(spec, m, dtype):
+    """The constant-coefficient instance of a built-in plan drops the zero terms
+    of the fold; for finite data the sums are unchanged, so it gives the same
+    bits as the run-time-coefficient instance."""
+    from paper_1905_05233_amd.winograd import Plan
+    N, H, W, C, K = _unrolled_shape(m, dtype, ragged_k=False)
+    x, w = _inputs((N, H, W, C, K), dtype, seed=m)
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
+    pb = Plan(spec, m=m, dtype=dtype, path="fused")
+    pr = Plan(spec, m=m, dtype=dtype, path="fused", generic_transforms=True)
+    assert pb.builtin >= 0 and pr.builtin < 0
+    U, V = pb.kernel_input_transform(wd, xd)
+    yb = pb.contract_output(V, U, C, N, H, W)
+    yr = pr.contract_output(V, U, C, N, H, W)
+    torch.cuda.synchronize()
+    assert torch.equal(yb, yr)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
 def test_stage_entry_point(dtype):
     """winograd_contract_output on the transforms' outputs is conv2d's fused path."""

@@ -187,13 +187,90 @@ _Zk:                                    ; @_Zk
     assert lds_read_hazards(vmem) == (1, [("_Zk", "v_mov_b32_e32 v21, v17")])
 
 
-@pytest.mark.skipif(not os.path.exists(B.HIPCC), reason="hipcc not installed")
-@pytest.mark.parametrize("source,dtypes,min_kernels", [("fused", (0, 1, 2), 40)])
-def test_kernels_wait_before_using_lds_fragments(source, dtypes, min_kernels, tmp_path):
-    """One build per storage dtype (the source is compiled with WG_DTYPE set)."""
+@pytest.fixture(scope="module")
+def fused_asm(tmp_path_factory):
+    """gfx950 assembly of fused.hip, one build per storage dtype (the source is
+    compiled with WG_DTYPE set)."""
+    if not os.path.exists(B.HIPCC):
+        pytest.skip("hipcc not installed")
+    out = str(tmp_path_factory.mktemp("fused_asm"))
     with ThreadPoolExecutor(3) as ex:
-        asms = list(ex.map(lambda d: _device_asm(source, d, str(tmp_path)), dtypes))
-    for code, asm in zip(dtypes, asms):
+        return dict(zip((0, 1, 2), ex.map(lambda d: _device_asm("fused", d, out), (0, 1, 2))))
+
+
+def test_kernels_wait_before_using_lds_fragments(fused_asm):
+    for code, asm in fused_asm.items():
         kernels, hits = lds_read_hazards(asm)
-        assert kernels >= min_kernels, f"{source} dtype {code}: only {kernels} kernels found in the assembly"
-        assert not hits, f"{source} dtype {code}: {len(hits)} uses of in-flight LDS fragments, e.g. {hits[:3]}"
+        assert kernels >= 40, f"fused dtype {code}: only {kernels} kernels found in the assembly"
+        assert not hits, f"fused dtype {code}: {len(hits)} uses of in-flight LDS fragments, e.g. {hits[:3]}"
+
+
+def stage_wait_violations(kernel_code, per_step, steps):
+    """For a kernel whose first ``steps`` workgroup barriers each begin a step,
+    and whose buffer-to-LDS loads fill the stages in step order, ``per_step``
+    loads per wave and step: the steps at which the last vmcnt wait before the
+    barrier does not cover that step's loads, as (step, vector-memory
+    operations issued after the step's last load, wait)."""
+    vm, nbar, wait, bad = [], 0, None, []
+    for line in kernel_code.split("\n"):
+        s = line.strip()
+        if not s or s.startswith((";", ".")):
+            continue
+        ins = s.split(";")[0].strip()
+        if ins.startswith(("buffer_load", "global_load")):
+            vm.append(ins.endswith(" lds"))
+        m = re.match(r"s_waitcnt.*vmcnt\((\d+)\)", ins)
+        if m:
+            wait = int(m.group(1))
+        if ins.startswith("s_barrier") and nbar < steps:
+            lds = [i for i, is_lds in enumerate(vm) if is_lds]
+            last = (nbar + 1) * per_step - 1
+            after = len(vm) - 1 - lds[last] if last < len(lds) else -1
+            if wait is None or after < wait:
+                bad.append((nbar, after, wait))
+            nbar += 1
+            wait = None
+    return nbar, bad
+
+
+def test_scanner_counts_stage_waits():
+    """The stage-wait scanner on hand-written code: the load of step 1 needs
+    two younger loads when the wait allows two outstanding."""
+    ok = """
+\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds
+\tbuffer_load_dwordx4 v1, s[8:11], 0 offen lds
+\tbuffer_load_dwordx4 v[2:5], v6, s[0:3], 0 offen
+\ts_waitcnt vmcnt(2)
+\ts_barrier
+\tbuffer_load_dwordx4 v[8:11], v6, s[0:3], 0 offen
+\ts_waitcnt vmcnt(2)
+\ts_barrier
+"""
+    assert stage_wait_violations(ok, 1, 2) == (2, [])
+    assert stage_wait_violations(ok.replace("vmcnt(2)\n\ts_barrier\n\tbuffer_load_dwordx4 v[8:11]",
+                                            "vmcnt(3)\n\ts_barrier\n\tbuffer_load_dwordx4 v[8:11]"), 1, 2) == (2, [(0, 2, 3)])
+    # two loads per step: the wait before the first barrier must cover both
+    assert stage_wait_violations(ok, 2, 1) == (1, [(0, 1, 2)])
+
+
+def test_unrolled_kernels_wait_for_their_stage(fused_asm):
+    """The unrolled kernels count their own vmcnt waits: before step s's
+    barrier, this wave's buffer-to-LDS loads of step s (3 per 128-byte slice,
+    the s-th group in issue order) must have completed, i.e. at least as many
+    vector-memory operations were issued after the group's last load as the
+    wait leaves outstanding.  The template arguments give alpha' (steps =
+    alpha'^2) and the slices per step."""
+    for code, asm in fused_asm.items():
+        body = asm[:asm.index("amdhsa.kernels")] if "amdhsa.kernels" in asm else asm
+        parts = re.split(r"\n(_Z\S+):[^\n]*\n", body)
+        seen = 0
+        for i in range(1, len(parts), 2):
+            m = re.search(r"contract_output_unrolled_kernelILi\d+ELi\d+ELi(\d+)E.*ELi(\d)EEEv", parts[i])
+            if not m:
+                continue
+            seen += 1
+            alpha, nsl = int(m.group(1)), int(m.group(2))
+            steps, bad = stage_wait_violations(parts[i + 1], 3 * nsl, alpha * alpha)
+            assert steps == alpha * alpha, f"dtype {code}: {parts[i][:80]}: {steps} step barriers"
+            assert not bad, f"dtype {code}: {parts[i][:80]}: stage loads not covered {bad[:3]}"
+        assert seen >= 16, f"dtype {code}: {seen} unrolled kernels"
