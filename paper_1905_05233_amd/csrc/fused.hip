@@ -544,7 +544,9 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
 // When a channel row fits NSL 128-byte slices (NSL = 1: C <= 64 in fp16/bf16,
 // C <= 32 in fp32; NSL = 2: twice that) and the block is 64 output channels x
 // 32 tiles (WT = 2), the contraction of a domain point is a single step of NSL
-// slices, and this variant unrolls the alpha'^2 steps at compile time: the
+// slices; rows of at most 64 bytes share one slice between XP = 128 / row
+// bytes domain points, as in the looped kernel's narrow steps.  This variant
+// unrolls the domain points at compile time: the
 // output-transform coefficients of every fold are constants (for a built-in
 // plan the zero terms disappear; for any other plan they are read from the
 // kernel arguments once), and no step bookkeeping is left.  Each step's U and
@@ -584,14 +586,17 @@ constexpr int groups_after(int s) {
     return issued - (s + 1);
 }
 
-template <int D, int MM, int ALPHA, class CO, int NSL>
+template <int D, int MM, int ALPHA, class CO, int NSL, int XP>
 __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
     const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, typename DTypeOf<D>::type* __restrict__ y,
     OutputTable tab, Geometry geo, int n_kb, int rb) {
     using Elem = typename DTypeOf<D>::type;
     using S = Storage<Elem>;
     constexpr int WT = 2;                  // two 16-tile blocks per wave
-    constexpr int NSTEPS = ALPHA * ALPHA;
+    constexpr int NPTS = ALPHA * ALPHA;    // domain points
+    constexpr int NSTEPS = (NPTS + XP - 1) / XP;
+    constexpr int PPR = 8 / XP;            // 16-byte pieces of a domain point's row in a slice
+    static_assert(XP == 1 || NSL == 1, "narrow rows fit one slice");
     constexpr int NST = unrolled_stages<NSL>();
     constexpr int kSB = unrolled_stage_bytes<NSL>();
     constexpr int kKD = 3 * NSL;           // DMA instructions per wave and step
@@ -621,13 +626,17 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
     // DMA map (the looped kernel's): instruction j of wave w fills stage rows
     // 8 (w + 4 j) .. + 7 of each slice, channel rows 0 .. 63 first, then tile
     // rows; lane l lands at row 8 (w + 4 j) + l / 8, 16-byte column l % 8, and
-    // fetches piece (l % 8) ^ (l / 8) of its row; pieces past the row read zero
+    // fetches piece lp = (l % 8) ^ (l / 8) of the slice; pieces past the row
+    // read zero.  Narrow rows: piece lp holds byte 16 (lp % PPR) of the row of
+    // the step's domain point lp / PPR.
     const int lp = (lane & 7) ^ (lane >> 3);
+    const int lxi = lp / PPR;
+    const int piece = (lp % PPR) * 16;
     uint32_t roff[3];
 #pragma unroll
     for (int j = 0; j < 3; ++j) {
         const int row = 8 * (wave + 4 * j) + (lane >> 3);
-        roff[j] = static_cast<uint32_t>((row < 64 ? row : row - 64) * rb + lp * 16);
+        roff[j] = static_cast<uint32_t>((row < 64 ? row : row - 64) * rb + piece);
     }
     // descriptors over one plane's rows of the block (rows past K or T read zero)
     const unsigned char* bu = U + k0 * rb;
@@ -637,9 +646,28 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
     const int rec_u = static_cast<int>(static_cast<uint32_t>(rec_u64 > 0xffffffffLL ? 0xffffffffLL : rec_u64));
     const int rec_v = static_cast<int>(static_cast<uint32_t>(rec_v64 > 0xffffffffLL ? 0xffffffffLL : rec_v64));
 
-    // step s is the domain point (a, b) = (s % alpha', s / alpha'), xi = a alpha' + b
+    // domain point q is (a, b) = (q % alpha', q / alpha'), xi = a alpha' + b;
+    // step s holds q = s XP .. s XP + XP - 1
+    // narrow: descriptors over every plane (the launcher checks that they fit
+    // 32-bit offsets); rows past T or K then read other planes' rows, which
+    // only reach (channel, tile) pairs that are never stored
+    const auto ru_all = make_rsrc(bu, (static_cast<int64_t>(NPTS) * K - k0) * rb);
+    const auto rv_all = make_rsrc(bv, (static_cast<int64_t>(NPTS) * T - t0) * rb);
     auto issue = [&](auto sc) __attribute__((always_inline)) {
         constexpr int s = decltype(sc)::value;
+        if constexpr (XP > 1) {
+            const int q = s * XP + lxi;
+            const int pxi = (q % ALPHA) * ALPHA + q / ALPHA;
+            const bool in = q < NPTS && piece < rb;
+            const uint32_t pu = static_cast<uint32_t>(pxi) * static_cast<uint32_t>(plane_u);
+            const uint32_t pv = static_cast<uint32_t>(pxi) * static_cast<uint32_t>(plane_v);
+            unsigned char* st = lds + (s % NST) * kSB;
+#pragma unroll
+            for (int j = 0; j < 3; ++j)
+                dma16(j < 2 ? ru_all : rv_all, st + (wave + 4 * j) * 1024,
+                      in ? roff[j] + (j < 2 ? pu : pv) : kOob);
+            return;
+        }
         constexpr uint64_t xi = (s % ALPHA) * ALPHA + s / ALPHA;
         const auto ru = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(bu + xi * plane_u),
                                                           static_cast<short>(0), rec_u, static_cast<int>(kRsrcWord3));
@@ -648,7 +676,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
         unsigned char* st = lds + (s % NST) * kSB;
 #pragma unroll
         for (int sl = 0; sl < NSL; ++sl) {
-            const bool in = sl * kSlice + lp * 16 < rb;
+            const bool in = sl * kSlice + piece < rb;
 #pragma unroll
             for (int j = 0; j < 3; ++j)
                 dma16(j < 2 ? ru : rv, st + sl * kStageBytes + (wave + 4 * j) * 1024,
@@ -721,6 +749,29 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
         lds_barrier();
         if constexpr (s + NST - 1 < NSTEPS) issue(std::integral_constant<int, s + NST - 1>{});
         const unsigned char* cur = lds + (s % NST) * kSB;
+        if constexpr (XP > 1) {
+            // domain point q of the step sits in pieces [i PPR, i PPR + PPR) of
+            // one slice half; lane groups outside them contribute zeros
+            unroll<XP>([&](auto ic) __attribute__((always_inline)) {
+                constexpr int i = decltype(ic)::value;
+                constexpr int q = s * XP + i;
+                if constexpr (q < NPTS) {
+                    constexpr int p0 = i * PPR;
+                    const int col = (((p0 & 4) + grp) ^ swz) * 16;
+                    u32x4 fa = lds_read16(cur + a_row + col);
+                    u32x4 fb0 = lds_read16(cur + b_row + col);
+                    u32x4 fb1 = lds_read16(cur + b_row + 16 * kSlice + col);
+                    if constexpr (q > 0) fold(std::integral_constant<int, q - 1>{});
+                    lds_settle(fa, fb0, fb1);
+                    if (static_cast<unsigned>(grp - (p0 & 3)) >= static_cast<unsigned>(PPR)) fa = u32x4{0u, 0u, 0u, 0u};
+                    part[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                    part[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                    mma<D>(fa, fb0, part[0]);
+                    mma<D>(fa, fb1, part[1]);
+                }
+            });
+            return;
+        }
         u32x4 fa0 = lds_read16(cur + a_row + col0);
         u32x4 fa1 = lds_read16(cur + a_row + col1);
         u32x4 fb00 = lds_read16(cur + b_row + col0);
@@ -758,7 +809,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
         if constexpr (decltype(sc)::value < NSTEPS) issue(sc);
     });
     unroll<NSTEPS>(step);
-    fold(std::integral_constant<int, NSTEPS - 1>{});
+    fold(std::integral_constant<int, NPTS - 1>{});
     // the output tile is complete here: without this, the compiler sinks the
     // folds of every step into the (conditional) store code after the loop
 #pragma unroll
@@ -924,12 +975,15 @@ hipError_t launch_co_instance(const CoArgs& c, hipStream_t stream) {
 template <int D, int TT, int A, class CO>
 hipError_t launch_unrolled_instance(const CoArgs& c, hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
-    if (c.n_slices == 1)
-        hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, 1>), dim3(c.nb), dim3(kThreads), 0,
-                           stream, c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.n_kb, c.rb);
-    else
-        hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, 2>), dim3(c.nb), dim3(kThreads), 0,
-                           stream, c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.n_kb, c.rb);
+#define WG_UNR_LAUNCH(NSL, XP)                                                                                  \
+    hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, NSL, XP>), dim3(c.nb), dim3(kThreads), \
+                       0, stream, c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.n_kb, c.rb)
+    if (c.xp == 8) WG_UNR_LAUNCH(1, 8);
+    else if (c.xp == 4) WG_UNR_LAUNCH(1, 4);
+    else if (c.xp == 2) WG_UNR_LAUNCH(1, 2);
+    else if (c.n_slices == 1) WG_UNR_LAUNCH(1, 1);
+    else WG_UNR_LAUNCH(2, 1);
+#undef WG_UNR_LAUNCH
     return hipGetLastError();
 }
 
@@ -968,8 +1022,8 @@ hipError_t launch_co(const Geometry& g, const OutputTable& tab, const void* V, c
     if (itab) c.itab = *itab;
     else std::memset(&c.itab, 0, sizeof(c.itab));
     c.nb = static_cast<unsigned>(grid);
-    if (!x && xp == 1 && c.n_slices <= 2 && wt == 2 && kw == 4) {
-        // one step per domain point, blocks of 64 output channels x 32 tiles
+    if (!x && c.n_slices <= 2 && wt == 2 && kw == 4) {
+        // whole rows per step, blocks of 64 output channels x 32 tiles
         switch (builtin) {
 #define WG_UNR_BUILTIN(ID, TT, A)                                                                          \
     case ID:                                                                                               \

@@ -137,12 +137,14 @@ UNROLLED_PLANS = [
 ]
 
 
-def _unrolled_shape(m, dtype, ragged_k, slices=1):
+def _unrolled_shape(m, dtype, ragged_k, slices=1, C=None):
     """A layer the launcher sends to the unrolled kernel: rows that leave the
     last pieces of a 128-byte slice empty, or fill it; ragged tiles; with
     ``ragged_k`` an output-channel count whose rows end mid 16-byte chunk (the
     epilogue's direct stores) and a partial block of 64 channels."""
-    if slices == 1:
+    if C is not None:
+        pass
+    elif slices == 1:
         C = {"f32": 20, "f16": 48, "bf16": 64}[dtype]
     else:
         C = {"f32": 48, "f16": 100, "bf16": 128}[dtype]
@@ -154,7 +156,7 @@ def _unrolled_shape(m, dtype, ragged_k, slices=1):
 def _selects_unrolled(m, C, K, T, dtype):
     rb = -(-C // 8) * 8 * (4 if dtype == "f32" else 2)
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    return m <= 4 and 64 < rb <= 256 and K > 32 and (-(-K // 64)) * (-(-T // 32)) >= 2 * cus
+    return m <= 4 and rb <= 256 and K > 32 and (-(-K // 64)) * (-(-T // 32)) >= 2 * cus
 
 
 def _gpu_stages(p, V, U, M, C, K, N, H, W):
@@ -166,9 +168,9 @@ def _gpu_stages(p, V, U, M, C, K, N, H, W):
             "M": to_np(M)[:, :, :K].reshape(al, al, N, th, tw, K)}
 
 
-def _unrolled_vs_separate(spec, m, generic, dtype, slices):
+def _unrolled_vs_separate(spec, m, generic, dtype, slices, C=None):
     from paper_1905_05233_amd.winograd import Plan
-    N, H, W, C, K = _unrolled_shape(m, dtype, ragged_k=generic, slices=slices)
+    N, H, W, C, K = _unrolled_shape(m, dtype, ragged_k=generic, slices=slices, C=C)
     print(f"[unrolled] {spec} m={m} generic={generic} {dtype} {(N, H, W, C, K)}", flush=True)
     x, w = _inputs((N, H, W, C, K), dtype, seed=5 * m + C)
     p = Plan(spec, m=m, dtype=dtype, path="fused", generic_transforms=generic)
@@ -215,6 +217,23 @@ UNROLLED_TWO_SLICES = [(WL.F2_LINEAR, 2, False), (WL.F4_A2P1, 4, False), (WL.F4_
 def test_unrolled_two_slices_matches_separate(spec, m, generic, dtype):
     """The same with channel rows of two slices (a step contracts both)."""
     _unrolled_vs_separate(spec, m, generic, dtype, slices=2)
+
+
+# narrow rows: 128 / row bytes domain points share a step (8, 4 or 2)
+UNROLLED_NARROW = [
+    (WL.F4_A2P1, 4, False, "bf16", 3),       # 16-byte rows (the RGB layer): 8 per step
+    (WL.F4_A2P1, 4, True, "f16", 16),        # 32-byte rows: 4 per step
+    (WL.F2_LINEAR, 2, False, "f32", 12),     # 12 channels padded to 16: 64-byte rows, 2 per step
+    ("0,a^2+1,a^2-2,inf", 4, False, "bf16", 24),   # 48-byte rows: the last piece of each half empty
+    (WL.F4_LINEAR, 4, False, "f32", 4),      # 32-byte rows in fp32
+]
+
+
+@pytest.mark.parametrize("spec,m,generic,dtype,C", UNROLLED_NARROW,
+                         ids=[f"{s}-m{m}-{d}-C{c}" + ("-runtime" if g else "") for s, m, g, d, c in UNROLLED_NARROW])
+def test_unrolled_narrow_matches_separate(spec, m, generic, dtype, C):
+    """The same with rows of at most 64 bytes, several domain points per step."""
+    _unrolled_vs_separate(spec, m, generic, dtype, slices=1, C=C)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

@@ -258,19 +258,21 @@ def test_unrolled_kernels_wait_for_their_stage(fused_asm):
     barrier, this wave's buffer-to-LDS loads of step s (3 per 128-byte slice,
     the s-th group in issue order) must have completed, i.e. at least as many
     vector-memory operations were issued after the group's last load as the
-    wait leaves outstanding.  The template arguments give alpha' (steps =
-    alpha'^2) and the slices per step."""
+    wait leaves outstanding.  The template arguments give alpha', the
+    slices per step and the domain points per step (steps = alpha'^2 / that,
+    rounded up)."""
     for code, asm in fused_asm.items():
         body = asm[:asm.index("amdhsa.kernels")] if "amdhsa.kernels" in asm else asm
         parts = re.split(r"\n(_Z\S+):[^\n]*\n", body)
         seen = 0
         for i in range(1, len(parts), 2):
-            m = re.search(r"contract_output_unrolled_kernelILi\d+ELi\d+ELi(\d+)E.*ELi(\d)EEEv", parts[i])
+            m = re.search(r"contract_output_unrolled_kernelILi\d+ELi\d+ELi(\d+)E.*ELi(\d)ELi(\d)EEEv", parts[i])
             if not m:
                 continue
             seen += 1
-            alpha, nsl = int(m.group(1)), int(m.group(2))
-            steps, bad = stage_wait_violations(parts[i + 1], 3 * nsl, alpha * alpha)
-            assert steps == alpha * alpha, f"dtype {code}: {parts[i][:80]}: {steps} step barriers"
+            alpha, nsl, xp = int(m.group(1)), int(m.group(2)), int(m.group(3))
+            n = -(-alpha * alpha // xp)
+            steps, bad = stage_wait_violations(parts[i + 1], 3 * nsl, n)
+            assert steps == n, f"dtype {code}: {parts[i][:80]}: {steps} step barriers"
             assert not bad, f"dtype {code}: {parts[i][:80]}: stage loads not covered {bad[:3]}"
-        assert seen >= 16, f"dtype {code}: {seen} unrolled kernels"
+        assert seen >= 40, f"dtype {code}: {seen} unrolled kernels"
