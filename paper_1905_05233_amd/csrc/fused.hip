@@ -545,8 +545,10 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
 // C <= 32 in fp32; NSL = 2: twice that) and the block is 64 output channels x
 // 32 tiles (WT = 2), the contraction of a domain point is a single step of NSL
 // slices; rows of at most 64 bytes share one slice between XP = 128 / row
-// bytes domain points, as in the looped kernel's narrow steps.  This variant
-// unrolls the domain points at compile time: the
+// bytes domain points, as in the looped kernel's narrow steps; longer rows
+// (CH) take n_ch steps of one slice per domain point, in a loop at run time,
+// their MFMA chains accumulating over the steps.  This variant unrolls the
+// domain points at compile time: the
 // output-transform coefficients of every fold are constants (for a built-in
 // plan the zero terms disappear; for any other plan they are read from the
 // kernel arguments once), and no step bookkeeping is left.  Each step's U and
@@ -586,10 +588,10 @@ constexpr int groups_after(int s) {
     return issued - (s + 1);
 }
 
-template <int D, int MM, int ALPHA, class CO, int NSL, int XP>
+template <int D, int MM, int ALPHA, class CO, int NSL, int XP, bool CH>
 __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
     const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, typename DTypeOf<D>::type* __restrict__ y,
-    OutputTable tab, Geometry geo, int n_kb, int rb) {
+    OutputTable tab, Geometry geo, int n_kb, int rb, int n_ch) {
     using Elem = typename DTypeOf<D>::type;
     using S = Storage<Elem>;
     constexpr int WT = 2;                  // two 16-tile blocks per wave
@@ -597,6 +599,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
     constexpr int NSTEPS = (NPTS + XP - 1) / XP;
     constexpr int PPR = 8 / XP;            // 16-byte pieces of a domain point's row in a slice
     static_assert(XP == 1 || NSL == 1, "narrow rows fit one slice");
+    static_assert(!CH || (NSL == 1 && XP == 1), "long rows go in steps of one slice");
     constexpr int NST = unrolled_stages<NSL>();
     constexpr int kSB = unrolled_stage_bytes<NSL>();
     constexpr int kKD = 3 * NSL;           // DMA instructions per wave and step
@@ -728,6 +731,27 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
 #pragma unroll
                     for (int r = 0; r < 4; ++r) Z[w][o][r] = 0.0f;
         }
+        if constexpr (CH) {
+            // the fold happens here: the compiler would otherwise sink it past
+            // the run-time loops of later domain points, keeping every
+            // domain point's M live
+#pragma unroll
+            for (int w = 0; w < WT; ++w)
+#pragma unroll
+                for (int o = 0; o < MM; ++o)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) asm volatile("" : "+v"(Z[w][o][r]));
+            if constexpr (a == ALPHA - 1) {
+#pragma unroll
+                for (int w = 0; w < WT; ++w)
+#pragma unroll
+                    for (int o = 0; o < MM; ++o)
+#pragma unroll
+                        for (int q = 0; q < MM; ++q)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) asm volatile("" : "+v"(Y[w][o][q][r]));
+            }
+        }
     };
 
     // fragments: A = channel row 16 wave + l16, B = tile row 16 w + l16 of
@@ -804,12 +828,79 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
         }
     };
 
-    // prologue: steps 0 .. NST-2 requested
-    unroll<NST - 1>([&](auto sc) __attribute__((always_inline)) {
-        if constexpr (decltype(sc)::value < NSTEPS) issue(sc);
-    });
-    unroll<NSTEPS>(step);
-    fold(std::integral_constant<int, NPTS - 1>{});
+    if constexpr (CH) {
+        // Long rows: step (q, c) is slice c of domain point q, steps in the
+        // order q n_ch + c.  The request for the step NST - 1
+        // ahead is tracked by counters (rq, rc) and its stage rs; past the last
+        // step a group of out-of-range requests (zero fills) keeps one group
+        // per step, so every step waits for the same count.
+        int rq = 0, rc = 0, rs = 0, cs = 0;
+        auto issue_next = [&]() __attribute__((always_inline)) {
+            const bool live = rq < NPTS;
+            const uint64_t xi = live ? static_cast<uint64_t>((rq % ALPHA) * ALPHA + rq / ALPHA) : 0;
+            const auto ru = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(bu + xi * plane_u),
+                                                              static_cast<short>(0), rec_u,
+                                                              static_cast<int>(kRsrcWord3));
+            const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(bv + xi * plane_v),
+                                                              static_cast<short>(0), rec_v,
+                                                              static_cast<int>(kRsrcWord3));
+            unsigned char* st = lds + rs * kSB;
+            const int sb = rc * kSlice;
+            const bool in = live && sb + piece < rb;
+#pragma unroll
+            for (int j = 0; j < 3; ++j)
+                dma16(j < 2 ? ru : rv, st + (wave + 4 * j) * 1024, in ? roff[j] + sb : kOob);
+            if (++rc == n_ch) {
+                rc = 0;
+                ++rq;
+            }
+            rs = rs + 1 == NST ? 0 : rs + 1;
+        };
+        // one step: wait for this wave's group of the step, barrier, request
+        // the group NST - 1 ahead, contract the slice into part
+        auto chunk = [&](auto qc, bool first) __attribute__((always_inline)) {
+            constexpr int q = decltype(qc)::value;
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_waitcnt(vm_wait(kKD * (NST - 2)));
+            lds_barrier();
+            issue_next();
+            const unsigned char* cur = lds + cs * kSB;
+            cs = cs + 1 == NST ? 0 : cs + 1;
+            u32x4 fa0 = lds_read16(cur + a_row + col0);
+            u32x4 fa1 = lds_read16(cur + a_row + col1);
+            u32x4 fb00 = lds_read16(cur + b_row + col0);
+            u32x4 fb01 = lds_read16(cur + b_row + col1);
+            u32x4 fb10 = lds_read16(cur + b_row + 16 * kSlice + col0);
+            u32x4 fb11 = lds_read16(cur + b_row + 16 * kSlice + col1);
+            if (first) {
+                if constexpr (q > 0) fold(std::integral_constant<int, q - 1>{});
+            }
+            lds_settle(fa0, fa1, fb00, fb01, fb10, fb11);
+            if (first) {
+                part[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                part[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            }
+            mma<D>(fa0, fb00, part[0]);
+            mma<D>(fa0, fb10, part[1]);
+            mma<D>(fa1, fb01, part[0]);
+            mma<D>(fa1, fb11, part[1]);
+        };
+        for (int i = 0; i < NST - 1; ++i) issue_next();
+        unroll<NPTS>([&](auto qc) __attribute__((always_inline)) {
+            chunk(qc, true);   // the first chunk folds the previous domain point
+            for (int c = 1; c < n_ch; ++c) chunk(qc, false);
+        });
+        fold(std::integral_constant<int, NPTS - 1>{});
+        // the trailing zero-fill groups land before the LDS is reused
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+    } else {
+        // prologue: steps 0 .. NST-2 requested
+        unroll<NST - 1>([&](auto sc) __attribute__((always_inline)) {
+            if constexpr (decltype(sc)::value < NSTEPS) issue(sc);
+        });
+        unroll<NSTEPS>(step);
+        fold(std::integral_constant<int, NPTS - 1>{});
+    }
     // the output tile is complete here: without this, the compiler sinks the
     // folds of every step into the (conditional) store code after the loop
 #pragma unroll
@@ -975,14 +1066,16 @@ hipError_t launch_co_instance(const CoArgs& c, hipStream_t stream) {
 template <int D, int TT, int A, class CO>
 hipError_t launch_unrolled_instance(const CoArgs& c, hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
-#define WG_UNR_LAUNCH(NSL, XP)                                                                                  \
-    hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, NSL, XP>), dim3(c.nb), dim3(kThreads), \
-                       0, stream, c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.n_kb, c.rb)
-    if (c.xp == 8) WG_UNR_LAUNCH(1, 8);
-    else if (c.xp == 4) WG_UNR_LAUNCH(1, 4);
-    else if (c.xp == 2) WG_UNR_LAUNCH(1, 2);
-    else if (c.n_slices == 1) WG_UNR_LAUNCH(1, 1);
-    else WG_UNR_LAUNCH(2, 1);
+#define WG_UNR_LAUNCH(NSL, XP, CH)                                                                              \
+    hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, NSL, XP, CH>), dim3(c.nb),             \
+                       dim3(kThreads), 0, stream, c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.n_kb, c.rb,   \
+                       c.n_slices)
+    if (c.xp == 8) WG_UNR_LAUNCH(1, 8, false);
+    else if (c.xp == 4) WG_UNR_LAUNCH(1, 4, false);
+    else if (c.xp == 2) WG_UNR_LAUNCH(1, 2, false);
+    else if (c.n_slices == 1) WG_UNR_LAUNCH(1, 1, false);
+    else if (c.n_slices == 2) WG_UNR_LAUNCH(2, 1, false);
+    else WG_UNR_LAUNCH(1, 1, true);
 #undef WG_UNR_LAUNCH
     return hipGetLastError();
 }
@@ -1022,7 +1115,7 @@ hipError_t launch_co(const Geometry& g, const OutputTable& tab, const void* V, c
     if (itab) c.itab = *itab;
     else std::memset(&c.itab, 0, sizeof(c.itab));
     c.nb = static_cast<unsigned>(grid);
-    if (!x && c.n_slices <= 2 && wt == 2 && kw == 4) {
+    if (!x && wt == 2 && kw == 4) {
         // whole rows per step, blocks of 64 output channels x 32 tiles
         switch (builtin) {
 #define WG_UNR_BUILTIN(ID, TT, A)                                                                          \

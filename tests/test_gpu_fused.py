@@ -108,7 +108,7 @@ def test_fused_matches_separate(spec, m, dtype):
 
 
 # VGG-16 layers that the automatic rule sends to the fused kernel (N = 1)
-VGG_FUSED = [(224, 3, 64), (224, 64, 64), (112, 64, 128), (112, 128, 128), (56, 128, 256)]
+VGG_FUSED = [(224, 3, 64), (224, 64, 64), (112, 64, 128), (112, 128, 128), (56, 128, 256), (56, 256, 256)]
 
 
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
@@ -156,7 +156,7 @@ def _unrolled_shape(m, dtype, ragged_k, slices=1, C=None):
 def _selects_unrolled(m, C, K, T, dtype):
     rb = -(-C // 8) * 8 * (4 if dtype == "f32" else 2)
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    return m <= 4 and rb <= 256 and K > 32 and (-(-K // 64)) * (-(-T // 32)) >= 2 * cus
+    return m <= 4 and K > 32 and (-(-K // 64)) * (-(-T // 32)) >= 2 * cus
 
 
 def _gpu_stages(p, V, U, M, C, K, N, H, W):
@@ -217,6 +217,22 @@ UNROLLED_TWO_SLICES = [(WL.F2_LINEAR, 2, False), (WL.F4_A2P1, 4, False), (WL.F4_
 def test_unrolled_two_slices_matches_separate(spec, m, generic, dtype):
     """The same with channel rows of two slices (a step contracts both)."""
     _unrolled_vs_separate(spec, m, generic, dtype, slices=2)
+
+
+# long rows: one slice per step, the steps of a domain point in a loop
+UNROLLED_LONG = [
+    (WL.F4_A2P1, 4, False, "bf16", 256),     # 512-byte rows: 4 steps per domain point
+    (WL.F4_A2P1, 4, True, "f16", 200),       # 400-byte rows, the last step's slice partly empty
+    (WL.F2_LINEAR, 2, False, "f32", 100),    # 400-byte rows in fp32
+    ("0,a^2+1,a^2-2,inf", 4, False, "bf16", 520),   # 1040-byte rows: 9 steps
+]
+
+
+@pytest.mark.parametrize("spec,m,generic,dtype,C", UNROLLED_LONG,
+                         ids=[f"{s}-m{m}-{d}-C{c}" + ("-runtime" if g else "") for s, m, g, d, c in UNROLLED_LONG])
+def test_unrolled_long_rows_matches_separate(spec, m, generic, dtype, C):
+    """The same with rows longer than two slices."""
+    _unrolled_vs_separate(spec, m, generic, dtype, slices=1, C=C)
 
 
 # narrow rows: 128 / row bytes domain points share a step (8, 4 or 2)

@@ -253,6 +253,34 @@ def test_scanner_counts_stage_waits():
     assert stage_wait_violations(ok, 2, 1) == (1, [(0, 1, 2)])
 
 
+def test_scanner_checks_looped_stage_waits():
+    """The looped form's checker on a hand-written loop: one group of two
+    loads per step after a prologue of two groups (three stages); a wait that
+    leaves two groups outstanding, or a path that issues two groups between
+    barriers, is flagged."""
+    code = """
+_Zk:                                    ; @_Zk
+\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds
+\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds
+\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds
+\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds
+.LBB0_1:
+\ts_waitcnt vmcnt(2)
+\ts_barrier
+\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds
+\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds
+\ts_cbranch_scc1 .LBB0_1
+\ts_waitcnt vmcnt(0)
+\ts_barrier
+\ts_endpgm
+"""
+    assert chunked_wait_violations(code, 2, 3) == []
+    assert chunked_wait_violations(code.replace("vmcnt(2)", "vmcnt(4)"), 2, 3)
+    extra = code.replace("\ts_cbranch_scc1 .LBB0_1", "\ts_cbranch_scc1 .LBB0_1\n\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds\n"
+                         "\tbuffer_load_dwordx4 v1, s[4:7], 0 offen lds\n\ts_branch .LBB0_1")
+    assert chunked_wait_violations(extra, 2, 3)
+
+
 def test_unrolled_kernels_wait_for_their_stage(fused_asm):
     """The unrolled kernels count their own vmcnt waits: before step s's
     barrier, this wave's buffer-to-LDS loads of step s (3 per 128-byte slice,
@@ -266,13 +294,79 @@ def test_unrolled_kernels_wait_for_their_stage(fused_asm):
         parts = re.split(r"\n(_Z\S+):[^\n]*\n", body)
         seen = 0
         for i in range(1, len(parts), 2):
-            m = re.search(r"contract_output_unrolled_kernelILi\d+ELi\d+ELi(\d+)E.*ELi(\d)ELi(\d)EEEv", parts[i])
+            m = re.search(r"contract_output_unrolled_kernelILi\d+ELi\d+ELi(\d+)E.*ELi(\d)ELi(\d)ELb([01])EEEv",
+                          parts[i])
             if not m:
                 continue
             seen += 1
-            alpha, nsl, xp = int(m.group(1)), int(m.group(2)), int(m.group(3))
+            alpha, nsl, xp, ch = int(m.group(1)), int(m.group(2)), int(m.group(3)), m.group(4) == "1"
+            if ch:
+                bad = chunked_wait_violations(parts[i + 1], 3, 4)
+                assert not bad, f"dtype {code}: {parts[i][:80]}: {bad[:3]}"
+                continue
             n = -(-alpha * alpha // xp)
             steps, bad = stage_wait_violations(parts[i + 1], 3 * nsl, n)
             assert steps == n, f"dtype {code}: {parts[i][:80]}: {steps} step barriers"
             assert not bad, f"dtype {code}: {parts[i][:80]}: stage loads not covered {bad[:3]}"
-        assert seen >= 40, f"dtype {code}: {seen} unrolled kernels"
+        assert seen >= 48, f"dtype {code}: {seen} unrolled kernels"
+
+
+def chunked_wait_violations(kernel_code, per_step, stages):
+    """The unrolled kernel's long-row form runs its steps in loops, one group
+    of ``per_step`` buffer-to-LDS loads per step after ``stages - 1`` groups in
+    the prologue, and waits for the same count before every step's barrier.
+    On every path through the kernel's control-flow graph that requires: the
+    first barrier follows the prologue's groups, every later step barrier
+    follows exactly one group, and every step's wait leaves at most
+    ``stages - 2`` groups outstanding (so the step's own group, ``stages - 1``
+    behind the newest, has landed).  The steps end at the wait for every load
+    (vmcnt(0)) before the epilogue.  Returns the violations found."""
+    blocks = _blocks(kernel_code)
+    index = {label: k for k, (label, _) in enumerate(blocks)}
+    succ = []
+    for k, (_, ins) in enumerate(blocks):
+        nxt = []
+        last = ins[-1] if ins else ""
+        m = re.match(r"^s_c?branch\w*\s+(\.LBB\w+)", last)
+        if m:
+            nxt.append(index[m.group(1)])
+        if not last.startswith(("s_branch", "s_endpgm", "s_setpc")) and k + 1 < len(blocks):
+            nxt.append(k + 1)
+        succ.append(nxt)
+    # state: (barriers seen, loads since the last barrier, last vmcnt since it); "done" after the final wait
+    entry = [set() for _ in blocks]
+    entry[0].add((False, 0, None))
+    work, bad, steps = [0], [], 0
+    while work:
+        k = work.pop()
+        for st in list(entry[k]):
+            cur = st
+            for ins in blocks[k][1]:
+                if cur == "done":
+                    break
+                seen, loads, wait = cur
+                if ins.startswith(("buffer_load", "global_load")) and ins.endswith(" lds"):
+                    cur = (seen, loads + 1, wait)
+                    continue
+                m = re.match(r"s_waitcnt.*vmcnt\((\d+)\)", ins)
+                if m:
+                    n = int(m.group(1))
+                    cur = "done" if (n == 0 and seen) else (seen, loads, n)
+                    continue
+                if ins.startswith("s_barrier"):
+                    want = per_step * (stages - 1) if not seen else per_step
+                    if loads != want:
+                        bad.append(("loads before barrier", blocks[k][0], loads, want))
+                    if wait is None or wait > per_step * (stages - 2):
+                        bad.append(("wait", blocks[k][0], wait))
+                    steps += 1
+                    cur = (True, 0, None)
+            for j in succ[k]:
+                if cur not in entry[j]:
+                    entry[j].add(cur)
+                    work.append(j)
+        if len(bad) > 20:
+            break
+    if steps < 2:
+        bad.append(("steps", steps))
+    return bad
