@@ -369,7 +369,8 @@ def run_vgg(a):
 
 STAGE_TRACE_NAMES = {"kernel_input_transform": ("kernel_input_transform<", "kernel_transform<", "input_transform<"),
                      "contract": ("contract_stream_kernel<", "contract_kernel<", "contract_pairwise_kernel<"),
-                     "output_transform": ("output_transform<",), "contract_output": ("contract_output_kernel<",),
+                     "output_transform": ("output_transform<",),
+                     "contract_output": ("contract_output_kernel<", "contract_output_unrolled_kernel<"),
                      "kernel_transform": ("kernel_transform<",), "input_contract_output": ("contract_output_kernel<",)}
 
 
