@@ -41,9 +41,10 @@ if ROOT not in sys.path:
 METRIC = "direct-equiv conv TFLOP/s + MFMA util/HBM GB/s; rel-L2 err vs fp64 direct"
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"f32": 157.3, "f16": 2500.0, "bf16": 2500.0}
-KERNEL_NAMES = ("kernel_input_transform", "contract", "output_transform", "contract_output", "kernel_transform",
-                "input_contract_output")
-KERNEL_SOURCES = {"kernel_input_transform": "transforms.hip", "contract": "contract.hip",
+KERNEL_NAMES = ("kernel_input_transform", "input_transform", "contract", "output_transform", "contract_output",
+                "kernel_transform", "input_contract_output")
+KERNEL_SOURCES = {"kernel_input_transform": "transforms.hip", "input_transform": "transforms.hip",
+                  "contract": "contract.hip",
                   "output_transform": "transforms.hip", "contract_output": "fused.hip",
                   "kernel_transform": "transforms.hip", "input_contract_output": "fused.hip"}
 
@@ -59,6 +60,8 @@ def algorithmic_work(wl, alpha, m):
         # one launch: kernel transform (w in, U out) and input transform (x in, V out)
         "kernel_input_transform": {"bytes": 9 * C * K * s + a2 * C * K * s + wl.N * wl.H * wl.W * C * s
                                    + a2 * T * C * s},
+        # later chunks of a chunked fused layer: the input transform alone
+        "input_transform": {"bytes": wl.N * wl.H * wl.W * C * s + a2 * T * C * s},
         "contract": {"flops": 2 * a2 * T * C * K, "bytes": a2 * (T * C * s + K * C * s + T * K * 4)},
         "output_transform": {"bytes": a2 * T * K * 4 + wl.N * wl.H * wl.W * K * s},
         # fused: V and U in, y out, no M
@@ -77,9 +80,23 @@ def source_hash(name):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def load_traffic(kernel, workload_tag):
+def load_traffic(kernel, workload_tag, layer=None):
     """HBM bytes per launch from committed rocprofv3 counter summaries, if they
-    were taken on the current kernel source; else None."""
+    were taken on the current kernel source; else None.  ``layer`` looks the
+    launch up in the stack's per-layer table (``traffic_{tag}.json``)."""
+    if layer is not None:
+        path = os.path.join(ROOT, "profiles", f"traffic_{workload_tag}.json")
+        if not os.path.exists(path):
+            return None
+        with open(path) as f:
+            tab = json.load(f)
+        src = KERNEL_SOURCES[kernel]
+        if tab.get("sources", {}).get(src) != source_hash(src):
+            return None
+        for e in tab.get("entries", []):
+            if e["layer"] == layer and e["kernel"] == kernel:
+                return e["hbm_bytes_per_launch"]
+        return None
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_tag}_traffic.json")
     if not os.path.exists(path):
         return None
@@ -90,13 +107,36 @@ def load_traffic(kernel, workload_tag):
     return rec.get("hbm_bytes_per_launch")
 
 
+def stage_counts(plan, N_, H, W, C, K):
+    """{stage: (images per launch, launches per conv2d)} for the launches
+    conv2d makes on this layer: a fused layer whose batch goes in chunks runs
+    the kernel and input transforms on the first chunk, the input transform
+    alone on each later one, and the fused kernel on every chunk (figures for
+    a chunk of the largest size)."""
+    path = plan.conv_path(N_, H, W, C, K)
+    n_chunks, chunk = plan.conv_chunks(N_, H, W, C, K)
+    if path == "fused_input":
+        return {"kernel_transform": (N_, 1), "input_contract_output": (N_, 1)}
+    if path == "fused":
+        if n_chunks == 1:
+            return {"kernel_input_transform": (N_, 1), "contract_output": (N_, 1)}
+        return {"kernel_input_transform": (chunk, 1), "input_transform": (chunk, n_chunks - 1),
+                "contract_output": (chunk, n_chunks)}
+    return {"kernel_input_transform": (N_, 1), "contract": (N_, 1), "output_transform": (N_, 1)}
+
+
 def make_stages(plan, xd, wd, y, N_, H, W, C, K, stream):
     """Launchers of the stage kernels that conv2d runs for this layer (the
-    path the plan takes for the shape; intermediates allocated here), in
+    path the plan takes for the shape, each launch over as many images as
+    conv2d gives it, see ``stage_counts``; intermediates allocated here), in
     launch order, each returning the library's status."""
     import torch
     from paper_1905_05233_amd import _native as NAT
     lib = NAT.lib()
+    counts = stage_counts(plan, N_, H, W, C, K)
+    if "input_transform" in counts:       # a chunked fused layer: launches over the first chunk
+        N_ = counts["contract_output"][0]
+        xd, y = xd[:N_], y[:N_]
     g = plan.geometry(N_, H, W, C, K)
     a2 = plan.alpha ** 2
     dev = xd.device
@@ -122,6 +162,9 @@ def make_stages(plan, xd, wd, y, N_, H, W, C, K, stream):
             plan._h, ctypes.byref(wt), ctypes.byref(xt), ctypes.c_void_p(U.data_ptr()), ctypes.c_void_p(V.data_ptr()),
             sh),
     }
+    if "input_transform" in counts:
+        stages["input_transform"] = lambda: lib.winograd_input_transform(
+            plan._h, ctypes.byref(xt), ctypes.c_void_p(V.data_ptr()), sh)
     if fused:
         stages["contract_output"] = lambda: lib.winograd_contract_output(
             plan._h, ctypes.c_void_p(V.data_ptr()), ctypes.c_void_p(U.data_ptr()), C, ctypes.byref(yt), sh)
@@ -251,17 +294,19 @@ def run_vgg(a):
         for li, (L, (xi, yi)) in enumerate(zip(stack.layers, trace)):
             y = torch.empty_like(yi)
             stages = make_stages(L["plan"], xi, L["w"], y, N, L["hw"], L["hw"], L["C"], L["K"], stream)
+            counts = stage_counts(L["plan"], N, L["hw"], L["hw"], L["C"], L["K"])
             for fn in stages.values():
                 NAT.check(fn())
             torch.cuda.synchronize()
-            work = _vgg_layer_work(L, N, dtype)
             for name, fn in stages.items():
+                work = _vgg_layer_work(L, counts[name][0], dtype)
                 for _ in range(a.steps):
                     NAT.check(fn())
                 torch.cuda.synchronize()
                 per = 2 if name == "kernel_input_transform" and L["plan"].tile_in > 8 else 1
                 order.append({"layer": li, "kernel": name, "launches": a.steps, "dispatches": a.steps * per,
                               "bytes": work[name]["bytes"], "flops": work[name].get("flops", 0),
+                              "images": counts[name][0], "per_conv": counts[name][1],
                               "shape": f"{L['hw']}x{L['hw']} {L['C']}->{L['K']}", "moduli": L["spec"].moduli})
         os.makedirs(os.path.dirname(os.path.abspath(a.order_out)), exist_ok=True)
         with open(a.order_out, "w") as f:
@@ -317,13 +362,15 @@ def run_vgg(a):
         hw, C, K = L["hw"], L["C"], L["K"]
         y = torch.empty_like(yi)
         stages = make_stages(L["plan"], xi, L["w"], y, N, hw, hw, C, K, stream)
+        counts = stage_counts(L["plan"], N, hw, hw, C, K)
         kus = time_kernels(stages, reps, stream)
-        work = _vgg_layer_work(L, N, dtype)
         for k, us in kus.items():
-            tot_us[k] += us
-            tot_work[k]["bytes"] += work[k]["bytes"]
-            tot_work[k]["flops"] += work[k].get("flops", 0)
-            launches.append((us, k, i, work[k]))
+            work = _vgg_layer_work(L, counts[k][0], dtype)[k]
+            n_launch = counts[k][1]
+            tot_us[k] += us * n_launch
+            tot_work[k]["bytes"] += work["bytes"] * n_launch
+            tot_work[k]["flops"] += work.get("flops", 0) * n_launch
+            launches.append((us, k, i, work))
         # accuracy of image 0 against the library's float64 direct convolution
         ref = layer_ops.direct_conv_f64(xi[:1], L["w"])
         err = layer_ops.rel_l2(yi[:1].contiguous(), ref)
@@ -331,11 +378,12 @@ def run_vgg(a):
                        "alpha": L["plan"].alpha, "path": L["plan"].conv_path(N, hw, hw, C, K),
                        "conv_ms": round(float(per_layer[i]), 4), "conv_ms_cold": round(float(cold[i]), 4),
                        "kernels_us": {k: round(v, 2) for k, v in kus.items()},
+                       "launches": {k: {"images": counts[k][0], "per_conv": counts[k][1]} for k in kus},
                        "rel_l2_image0": err})
     us, dom, dl, dwork = max(launches, key=lambda r: r[0])
     roof = roofline(dom, dwork, us, dtype)
     roof["layer"] = dl
-    roof["traffic"] = load_traffic(dom, f"vgg16_{dtype}_l{dl}")
+    roof["traffic"] = load_traffic(dom, f"vgg16_{dtype}", layer=dl)
     used = [k for k in KERNEL_NAMES if tot_us[k] > 0]
     kernels = {k: {"total_us": round(tot_us[k], 2), "algorithmic_bytes": tot_work[k]["bytes"],
                    "GB_s": round(tot_work[k]["bytes"] / (tot_us[k] * 1e-6) / 1e9, 1)} for k in used}
@@ -368,6 +416,7 @@ def run_vgg(a):
 
 
 STAGE_TRACE_NAMES = {"kernel_input_transform": ("kernel_input_transform<", "kernel_transform<", "input_transform<"),
+                     "input_transform": ("input_transform<",),
                      "contract": ("contract_stream_kernel<", "contract_kernel<", "contract_pairwise_kernel<"),
                      "output_transform": ("output_transform<",),
                      "contract_output": ("contract_output_kernel<", "contract_output_unrolled_kernel<"),
@@ -404,12 +453,13 @@ def _profile_groups(rows, info):
     return out
 
 
-def summarize_trace(trace_csv, order_json, counters=None):
+def summarize_trace(trace_csv, order_json, counters=None, table_out=None):
     """Markdown table (kernel x layer) of the average dispatch duration from a
     rocprofv3 kernel trace of ``bench.py --profile-kernel each``; with
     ``counters`` (FETCH_SIZE and WRITE_SIZE collections of the same mode and
     of the 256 MiB copy), also each group's HBM bytes per launch (medians,
-    scaled by the copy's true bytes over its readings)."""
+    scaled by the copy's true bytes over its readings), written as well to
+    ``table_out`` (JSON, with the kernel sources' hashes) for the bench line."""
     import statistics
     with open(order_json) as f:
         info = json.load(f)
@@ -433,8 +483,16 @@ def summarize_trace(trace_csv, order_json, counters=None):
         traffic = [statistics.median(float(r["Counter_Value"]) for r in f) * 1024 * rs
                    + statistics.median(float(r["Counter_Value"]) for r in w) * 1024 * ws for f, w in zip(fg, wg)]
     dt = info["dtype"]
-    head = "| layer | shape | kernel | dispatches | average (us) | algorithmic work | rate | fraction of peak |"
-    sep = "|---|---|---|---|---|---|---|---|"
+    if traffic and table_out:
+        entries = [{"layer": g["layer"], "kernel": g["kernel"], "images": g.get("images"),
+                    "algorithmic_bytes": g["bytes"], "hbm_bytes_per_launch": int(round(t))}
+                   for g, t in zip(info["order"], traffic)]
+        with open(table_out, "w") as f:
+            json.dump({"workload": f"vgg16_{dt}", "sources": {n: source_hash(n) for n in sorted(set(KERNEL_SOURCES.values()))},
+                       "read_scale": rs, "write_scale": ws, "entries": entries}, f, indent=1)
+    head = ("| layer | shape | kernel | images per launch, launches per conv | dispatches | average (us) | "
+            "algorithmic work | rate | fraction of peak |")
+    sep = "|---|---|---|---|---|---|---|---|---|"
     if traffic:
         head += " HBM bytes per launch (counters) | traffic / algorithmic |"
         sep += "---|---|"
@@ -445,12 +503,14 @@ def summarize_trace(trace_csv, order_json, counters=None):
         tot += us
         roof = roofline(g["kernel"], {"bytes": g["bytes"], "flops": g["flops"]}, us, dt)
         work = f"{g['bytes'] / 1e6:.1f} MB" + (f", {g['flops'] / 1e9:.2f} GFLOP" if g["flops"] else "")
-        line = (f"| {g['layer']} | {g['shape']} | `{g['kernel']}` | {g['dispatches']} | {us:.2f} | {work} | "
+        per = f"{g.get('images', '')}, {g.get('per_conv', '')}"
+        line = (f"| {g['layer']} | {g['shape']} | `{g['kernel']}` | {per} | {g['dispatches']} | {us:.2f} | {work} | "
                 f"{roof['achieved']} {roof['unit']} | {roof['frac']:.3f} ({roof['bound']}) |")
         if traffic:
             line += f" {traffic[gi] / 1e6:.1f} MB | {traffic[gi] / g['bytes']:.2f} |"
         lines.append(line)
-    lines.append(f"| all | | | | {tot:.2f} (sum over layers and kernels) |" + " |" * (len(sep.split("|")) - 7))
+    lines.append(f"| all | | | | | {tot:.2f} (sum over layers and kernels, one launch each) |"
+                 + " |" * (len(sep.split("|")) - 8))
     return "\n".join(lines)
 
 
@@ -531,12 +591,15 @@ def main(argv=None):
                     metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="print the traffic record of --profile-kernel from counter runs (no GPU)")
     ap.add_argument("--traffic-tag", default="vgg16_bf16_l1", help="workload tag of --summarize-counters")
+    ap.add_argument("--traffic-table-out", default=None,
+                    help="with --summarize-trace and counter files: also write the per-launch HBM bytes table (JSON)")
     a = ap.parse_args(argv)
 
     if a.summarize_trace:
         if len(a.summarize_trace) not in (2, 6, 7):
             ap.error("--summarize-trace takes 2, 6 or 7 files")
-        print(summarize_trace(a.summarize_trace[0], a.summarize_trace[1], a.summarize_trace[2:] or None))
+        print(summarize_trace(a.summarize_trace[0], a.summarize_trace[1], a.summarize_trace[2:] or None,
+                              a.traffic_table_out))
         return 0
     if a.summarize_counters:
         print(json.dumps(summarize_counters(a.profile_kernel, a.traffic_tag, *a.summarize_counters), indent=1))

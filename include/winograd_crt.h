@@ -204,7 +204,8 @@ wg_status winograd_plan_matrix_f32(wg_plan plan, char which, float* out, size_t 
 wg_status winograd_plan_ratio(wg_plan plan, int64_t* num, int64_t* den);
 
 /* Device workspace needed by winograd_conv2d for this layer shape (U and V,
- * plus M on the separate path). */
+ * plus M on the separate path; on the fused path V of one chunk of the batch
+ * when winograd_conv2d runs the batch in chunks, see there). */
 wg_status winograd_workspace_bytes(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C,
                                    int64_t K, size_t* bytes);
 
@@ -214,6 +215,13 @@ wg_status winograd_workspace_bytes(wg_plan plan, int64_t N, int64_t H, int64_t W
 wg_status winograd_conv_path(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C, int64_t K,
                              wg_conv_path* path);
 
+/* How winograd_conv2d splits the batch for this layer shape: n_chunks launch
+ * pairs (1 unless the fused path chunks the batch), the largest chunk having
+ * `chunk` images (the others one fewer at most).  WG_ERR_UNSUPPORTED as
+ * winograd_conv_path. */
+wg_status winograd_conv_chunks(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C, int64_t K,
+                               int64_t* n_chunks, int64_t* chunk);
+
 /* Bind a caller-owned device workspace (256-byte aligned) to the plan; a
  * NULL pointer unbinds.  The plan keeps the pointer, not the memory. */
 wg_status winograd_plan_set_workspace(wg_plan plan, void* dev_ptr, size_t bytes);
@@ -222,8 +230,13 @@ wg_status winograd_plan_set_workspace(wg_plan plan, void* dev_ptr, size_t bytes)
  * transform, then the alpha'^2 batched channel contraction and the output
  * transform (separate path) or the fused kernel that does both (fused path)
  * on `stream`, using the bound workspace; on WG_PATH_FUSED_INPUT the kernel
- * transform and the fused kernel that also computes V.  x is [N][H][W][C],
- * w is [K][3][3][C], y is [N][H][W][K]; N, H, W, C, K >= 1 (y->c = K). */
+ * transform and the fused kernel that also computes V.  On WG_PATH_FUSED a
+ * batch whose V would exceed 160 MiB goes through in chunks of whole images
+ * (sizes differing by at most one), the input transform and the fused kernel
+ * launched per chunk with one V buffer, so that V is read back from the
+ * GPU's last-level cache; the results are the same bits as one launch pair
+ * over the whole batch.  x is [N][H][W][C], w is [K][3][3][C], y is
+ * [N][H][W][K]; N, H, W, C, K >= 1 (y->c = K). */
 wg_status winograd_conv2d(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_tensor* y,
                           hipStream_t stream);
 

@@ -83,6 +83,7 @@ def lib():
         "winograd_workspace_bytes": (ctypes.c_int, [P, i64, i64, i64, i64, i64, ctypes.POINTER(sz)]),
         "winograd_plan_set_workspace": (ctypes.c_int, [P, P, sz]),
         "winograd_conv_path": (ctypes.c_int, [P, i64, i64, i64, i64, i64, ctypes.POINTER(ctypes.c_int)]),
+        "winograd_conv_chunks": (ctypes.c_int, [P, i64, i64, i64, i64, i64, ctypes.POINTER(i64), ctypes.POINTER(i64)]),
         "winograd_conv2d": (ctypes.c_int, [P, ctypes.POINTER(WgTensor), ctypes.POINTER(WgTensor),
                                            ctypes.POINTER(WgTensor), P]),
         "winograd_workspace_bytes_1d": (ctypes.c_int, [P, i64, i64, i64, i64, ctypes.POINTER(sz)]),

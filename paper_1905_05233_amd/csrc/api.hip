@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "builtin_plans.hpp"
+
 #include "kernels.hpp"
 #include "plan.hpp"
 #include "winograd_crt.h"
@@ -169,8 +170,16 @@ int resolve_path(const wg_plan_s* p, const wg::Geometry& g) {
 struct Layout {
     wg::Geometry g;
     int path;
+    int64_t n_chunks;   // launch pairs of the fused path: chunks of the batch, sizes differing by at most one
+    int64_t chunk;      // images of the largest chunk
     size_t u_off, v_off, m_off, total;
 };
+
+// On the fused path a large batch goes through in chunks of whole images
+// whose V is at most this size, one V buffer reused by every chunk: the input
+// transform writes a chunk's V and the fused kernel reads it back while it is
+// still in the GPU's 256 MB last-level cache, instead of from HBM.
+constexpr int64_t kChunkVBytes = int64_t(160) << 20;
 
 size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
@@ -180,8 +189,19 @@ Layout layout_for(const wg_plan_s* p, int64_t N, int64_t H, int64_t W, int64_t C
     L.path = resolve_path(p, L.g);
     const size_t es = static_cast<size_t>(wg::dtype_bytes(p->dtype));
     const size_t a2 = static_cast<size_t>(p->tr.alpha) * static_cast<size_t>(p->tr.alpha);
+    L.n_chunks = 1;
+    L.chunk = N;
+    if (L.path == WG_PATH_FUSED) {
+        // the fewest chunks within the budget, their sizes balanced
+        const int64_t v_img = static_cast<int64_t>(a2) * L.g.th * L.g.tw * L.g.Cp * static_cast<int64_t>(es);
+        if (v_img * N > kChunkVBytes) {
+            const int64_t per = std::max<int64_t>(1, kChunkVBytes / v_img);
+            L.n_chunks = (N + per - 1) / per;
+            L.chunk = (N + L.n_chunks - 1) / L.n_chunks;
+        }
+    }
     const size_t ub = a2 * static_cast<size_t>(K) * static_cast<size_t>(L.g.Cp) * es;
-    const size_t vb = a2 * static_cast<size_t>(L.g.T) * static_cast<size_t>(L.g.Cp) * es;
+    const size_t vb = a2 * static_cast<size_t>(L.chunk * L.g.th * L.g.tw) * static_cast<size_t>(L.g.Cp) * es;
     const size_t mb = a2 * static_cast<size_t>(L.g.T) * static_cast<size_t>(L.g.Kp) * sizeof(float);
     // no M on the fused paths, no V either when the input transform is fused
     L.u_off = 0;
@@ -463,6 +483,17 @@ wg_status winograd_conv_path(wg_plan plan, int64_t N, int64_t H, int64_t W, int6
     return WG_OK;
 }
 
+wg_status winograd_conv_chunks(wg_plan plan, int64_t N, int64_t H, int64_t W, int64_t C, int64_t K,
+                               int64_t* n_chunks, int64_t* chunk) {
+    if (!plan || !n_chunks || !chunk) return fail(WG_ERR_ARG, "null argument");
+    if (!dims_ok(N, H, W, C, K)) return fail(WG_ERR_ARG, "layer sizes must be in [1, 2^31)");
+    const Layout L = layout_for(plan, N, H, W, C, K);
+    if (L.path < 0) return fail(WG_ERR_UNSUPPORTED, "the fused path does not support this layer shape");
+    *n_chunks = L.n_chunks;
+    *chunk = L.chunk;
+    return WG_OK;
+}
+
 wg_status winograd_plan_set_workspace(wg_plan plan, void* dev_ptr, size_t bytes) {
     if (!plan) return fail(WG_ERR_ARG, "null plan");
     if (dev_ptr && (reinterpret_cast<uintptr_t>(dev_ptr) & 255u) != 0)
@@ -512,6 +543,26 @@ wg_status conv2d_with(wg_plan plan, const wg_tensor* x, const wg_tensor* w, wg_t
         if ((s = from_hip(launch_kt(dt, L.g, plan->ktab, w->data, U, stream), "kernel transform")) != WG_OK) return s;
         return from_hip(launch_ico(dt, L.g, plan->itab, plan->otab, x->data, U, y->data, stream),
                         "fused input transform and contraction");
+    }
+    if (L.path == WG_PATH_FUSED && L.n_chunks > 1) {
+        // chunks of images: the transforms of the first chunk compute U as well
+        const int64_t es = wg::dtype_bytes(dt);
+        const int64_t base = x->n / L.n_chunks, rem = x->n % L.n_chunks;
+        for (int64_t i = 0, n0 = 0; i < L.n_chunks; ++i) {
+            const int64_t nc = base + (i < rem ? 1 : 0);
+            const wg::Geometry g = wg::make_geometry(nc, x->h, x->w, x->c, w->n, plan->tr.m, plan->tr.alpha);
+            const void* xc = static_cast<const unsigned char*>(x->data) + n0 * x->h * x->w * x->c * es;
+            void* yc = static_cast<unsigned char*>(y->data) + n0 * y->h * y->w * y->c * es;
+            s = n0 == 0 ? from_hip(launch_kit(dt, g, plan->ktab, plan->itab, w->data, xc, U, V, plan->builtin, stream),
+                                   "kernel and input transforms")
+                        : from_hip(launch_it(dt, g, plan->itab, xc, V, plan->builtin, stream), "input transform");
+            if (s != WG_OK) return s;
+            if ((s = from_hip(launch_co(dt, g, plan->otab, V, U, yc, plan->builtin, stream), "fused contraction")) !=
+                WG_OK)
+                return s;
+            n0 += nc;
+        }
+        return WG_OK;
     }
     s = from_hip(launch_kit(dt, L.g, plan->ktab, plan->itab, w->data, x->data, U, V, plan->builtin, stream),
                  "kernel and input transforms");

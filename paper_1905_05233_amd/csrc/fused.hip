@@ -546,7 +546,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
 // 32 tiles (WT = 2), the contraction of a domain point is a single step of NSL
 // slices; rows of at most 64 bytes share one slice between XP = 128 / row
 // bytes domain points, as in the looped kernel's narrow steps; longer rows
-// (CH) take n_ch steps of one slice per domain point, in a loop at run time,
+// (CH) take n_ch steps of two slices per domain point, in a loop at run time,
 // their MFMA chains accumulating over the steps.  This variant unrolls the
 // domain points at compile time: the
 // output-transform coefficients of every fold are constants (for a built-in
@@ -599,7 +599,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
     constexpr int NSTEPS = (NPTS + XP - 1) / XP;
     constexpr int PPR = 8 / XP;            // 16-byte pieces of a domain point's row in a slice
     static_assert(XP == 1 || NSL == 1, "narrow rows fit one slice");
-    static_assert(!CH || (NSL == 1 && XP == 1), "long rows go in steps of one slice");
+    static_assert(!CH || (NSL == 2 && XP == 1), "long rows go in steps of two slices");
     constexpr int NST = unrolled_stages<NSL>();
     constexpr int kSB = unrolled_stage_bytes<NSL>();
     constexpr int kKD = 3 * NSL;           // DMA instructions per wave and step
@@ -829,8 +829,8 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
     };
 
     if constexpr (CH) {
-        // Long rows: step (q, c) is slice c of domain point q, steps in the
-        // order q n_ch + c.  The request for the step NST - 1
+        // Long rows: step (q, c) is chunk c (slices 2c and 2c + 1) of domain
+        // point q, steps in the order q n_ch + c.  The request for the step NST - 1
         // ahead is tracked by counters (rq, rc) and its stage rs; past the last
         // step a group of out-of-range requests (zero fills) keeps one group
         // per step, so every step waits for the same count.
@@ -845,11 +845,14 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
                                                               static_cast<short>(0), rec_v,
                                                               static_cast<int>(kRsrcWord3));
             unsigned char* st = lds + rs * kSB;
-            const int sb = rc * kSlice;
-            const bool in = live && sb + piece < rb;
 #pragma unroll
-            for (int j = 0; j < 3; ++j)
-                dma16(j < 2 ? ru : rv, st + (wave + 4 * j) * 1024, in ? roff[j] + sb : kOob);
+            for (int sl = 0; sl < NSL; ++sl) {
+                const int sb = (rc * NSL + sl) * kSlice;
+                const bool in = live && sb + piece < rb;
+#pragma unroll
+                for (int j = 0; j < 3; ++j)
+                    dma16(j < 2 ? ru : rv, st + sl * kStageBytes + (wave + 4 * j) * 1024, in ? roff[j] + sb : kOob);
+            }
             if (++rc == n_ch) {
                 rc = 0;
                 ++rq;
@@ -857,7 +860,7 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
             rs = rs + 1 == NST ? 0 : rs + 1;
         };
         // one step: wait for this wave's group of the step, barrier, request
-        // the group NST - 1 ahead, contract the slice into part
+        // the group NST - 1 ahead, contract both slices into part
         auto chunk = [&](auto qc, bool first) __attribute__((always_inline)) {
             constexpr int q = decltype(qc)::value;
             __builtin_amdgcn_sched_barrier(0);
@@ -880,6 +883,20 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
                 part[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
                 part[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
             }
+            mma<D>(fa0, fb00, part[0]);
+            mma<D>(fa0, fb10, part[1]);
+            mma<D>(fa1, fb01, part[0]);
+            mma<D>(fa1, fb11, part[1]);
+            // the second slice, its fragments read after the first slice's
+            // MFMAs have taken theirs (the register sets are reused)
+            cur += kStageBytes;
+            fa0 = lds_read16(cur + a_row + col0);
+            fa1 = lds_read16(cur + a_row + col1);
+            fb00 = lds_read16(cur + b_row + col0);
+            fb01 = lds_read16(cur + b_row + col1);
+            fb10 = lds_read16(cur + b_row + 16 * kSlice + col0);
+            fb11 = lds_read16(cur + b_row + 16 * kSlice + col1);
+            lds_settle(fa0, fa1, fb00, fb01, fb10, fb11);
             mma<D>(fa0, fb00, part[0]);
             mma<D>(fa0, fb10, part[1]);
             mma<D>(fa1, fb01, part[0]);
@@ -1005,9 +1022,11 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
 }
 
 // tile blocks per wave: as many as the output-tile registers allow (Y holds
-// m^2 values per channel-tile pair), fewer when that leaves CUs idle
+// m^2 values per channel-tile pair); with 64-channel blocks two (the unrolled
+// kernel's block), else fewer when that leaves CUs idle
 int pick_wt(const Geometry& g, int kw) {
     if (g.m > 4) return 1;
+    if (kw == 4) return 2;   // the unrolled kernel's block: 64 output channels x 32 tiles
     const int64_t n_kb = (g.K + 16 * kw - 1) / (16 * kw);
     const int64_t n_tb2 = (g.T + 16 * 2 * (4 / kw) - 1) / (16 * 2 * (4 / kw));
     return n_kb * n_tb2 >= 2 * device_cu_count() ? 2 : 1;
@@ -1069,13 +1088,13 @@ hipError_t launch_unrolled_instance(const CoArgs& c, hipStream_t stream) {
 #define WG_UNR_LAUNCH(NSL, XP, CH)                                                                              \
     hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, NSL, XP, CH>), dim3(c.nb),             \
                        dim3(kThreads), 0, stream, c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.n_kb, c.rb,   \
-                       c.n_slices)
+                       (c.n_slices + 1) / 2)
     if (c.xp == 8) WG_UNR_LAUNCH(1, 8, false);
     else if (c.xp == 4) WG_UNR_LAUNCH(1, 4, false);
     else if (c.xp == 2) WG_UNR_LAUNCH(1, 2, false);
     else if (c.n_slices == 1) WG_UNR_LAUNCH(1, 1, false);
     else if (c.n_slices == 2) WG_UNR_LAUNCH(2, 1, false);
-    else WG_UNR_LAUNCH(1, 1, true);
+    else WG_UNR_LAUNCH(2, 1, true);
 #undef WG_UNR_LAUNCH
     return hipGetLastError();
 }

@@ -151,6 +151,13 @@ class Plan:
         N.check(self._lib.winograd_conv_path(self._h, N_, H, W, C, K, ctypes.byref(out)))
         return N.PATH_NAMES[out.value]
 
+    def conv_chunks(self, N_, H, W, C, K):
+        """(launch pairs, images of the largest chunk) conv2d uses for this
+        layer: the fused path runs a large batch in chunks of images."""
+        n, c = ctypes.c_int64(), ctypes.c_int64()
+        N.check(self._lib.winograd_conv_chunks(self._h, N_, H, W, C, K, ctypes.byref(n), ctypes.byref(c)))
+        return n.value, c.value
+
     # ------------------------------------------------------------- compute
     @property
     def torch_dtype(self):

@@ -185,6 +185,28 @@ def test_exact_overflow_is_reported():
     assert ei.value.status in (6,)
 
 
+def test_conv_chunks_and_chunked_workspace():
+    """The fused path runs a batch whose V exceeds 160 MiB in balanced chunks
+    of images (winograd_conv_chunks), with a workspace of U and one chunk's
+    V; other layers run in one launch pair."""
+    p = Plan(WL.F4_A2P1, m=4, dtype="bf16")
+    v_img = 49 * 56 * 56 * 64 * 2                         # 224x224x64, F(4x4), alpha' = 7
+    per = (160 << 20) // v_img                            # 8 images within the budget
+    assert per == 8
+    assert p.conv_chunks(32, 224, 224, 64, 64) == (4, 8)
+    assert p.conv_chunks(9, 224, 224, 64, 64) == (2, 5)   # 5 + 4
+    assert p.conv_chunks(8, 224, 224, 64, 64) == (1, 8)
+    assert p.conv_chunks(32, 112, 112, 128, 128) == (2, 16)
+    u = -(-49 * 64 * 64 * 2 // 256) * 256
+    for n, chunk in ((32, 8), (9, 5), (8, 8)):
+        v = -(-49 * chunk * 56 * 56 * 64 * 2 // 256) * 256
+        assert p.workspace_bytes(n, 224, 224, 64, 64) == u + v
+    ps = Plan(WL.F4_A2P1, m=4, dtype="bf16", path="separate")
+    assert ps.conv_chunks(32, 224, 224, 64, 64) == (1, 32)
+    assert p.conv_path(32, 28, 28, 512, 512) == "separate"
+    assert p.conv_chunks(32, 28, 28, 512, 512) == (1, 32)
+
+
 def test_conv_path_option_and_workspace():
     """WG_PATH_SEPARATE / WG_PATH_FUSED / WG_PATH_AUTO: the resolved path and
     the workspace (the fused path needs no M), and the errors."""

@@ -219,12 +219,12 @@ def test_unrolled_two_slices_matches_separate(spec, m, generic, dtype):
     _unrolled_vs_separate(spec, m, generic, dtype, slices=2)
 
 
-# long rows: one slice per step, the steps of a domain point in a loop
+# long rows: two slices per step, the steps of a domain point in a loop
 UNROLLED_LONG = [
-    (WL.F4_A2P1, 4, False, "bf16", 256),     # 512-byte rows: 4 steps per domain point
-    (WL.F4_A2P1, 4, True, "f16", 200),       # 400-byte rows, the last step's slice partly empty
+    (WL.F4_A2P1, 4, False, "bf16", 256),     # 512-byte rows: 2 steps per domain point
+    (WL.F4_A2P1, 4, True, "f16", 200),       # 400-byte rows: the last step's second slice partly empty
     (WL.F2_LINEAR, 2, False, "f32", 100),    # 400-byte rows in fp32
-    ("0,a^2+1,a^2-2,inf", 4, False, "bf16", 520),   # 1040-byte rows: 9 steps
+    ("0,a^2+1,a^2-2,inf", 4, False, "bf16", 520),   # 1040-byte rows: 5 steps, the last one's second slice empty
 ]
 
 
@@ -270,6 +270,28 @@ def test_unrolled_builtin_equals_runtime_coefficients(spec, m, dtype):
     yr = pr.contract_output(V, U, C, N, H, W)
     torch.cuda.synchronize()
     assert torch.equal(yb, yr)
+
+
+@pytest.mark.parametrize("N", [9, 32])
+def test_conv2d_in_chunks_equals_one_launch(N):
+    """A batch whose V exceeds the chunk budget (224x224x64 -> 64, bf16: 19.7 MB
+    of V per image) runs as launch pairs over chunks of images (N = 9: 5 + 4,
+    N = 32: four of 8), with a workspace for one chunk's V; the output is the
+    fused kernel's over the whole batch, bit for bit."""
+    from paper_1905_05233_amd.winograd import Plan
+    H = W = 224
+    C = K = 64
+    x, w = _inputs((N, H, W, C, K), "bf16", seed=N)
+    p = Plan(WL.F4_A2P1, m=4, dtype="bf16")
+    assert p.conv_path(N, H, W, C, K) == "fused"
+    v_all = 49 * N * 56 * 56 * C * 2
+    assert p.workspace_bytes(N, H, W, C, K) < v_all        # one chunk's V, not the batch's
+    xd, wd = to_dev(x, "bf16"), to_dev(w, "bf16")
+    y = p.conv2d(xd, wd)
+    U, V = p.kernel_input_transform(wd, xd)
+    y_one = p.contract_output(V, U, C, N, H, W)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y_one)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])

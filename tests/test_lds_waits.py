@@ -301,7 +301,7 @@ def test_unrolled_kernels_wait_for_their_stage(fused_asm):
             seen += 1
             alpha, nsl, xp, ch = int(m.group(1)), int(m.group(2)), int(m.group(3)), m.group(4) == "1"
             if ch:
-                bad = chunked_wait_violations(parts[i + 1], 3, 4)
+                bad = chunked_wait_violations(parts[i + 1], 3 * nsl, 4 if nsl == 1 else 3)
                 assert not bad, f"dtype {code}: {parts[i][:80]}: {bad[:3]}"
                 continue
             n = -(-alpha * alpha // xp)
