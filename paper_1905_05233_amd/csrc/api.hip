@@ -159,12 +159,14 @@ int resolve_path(const wg_plan_s* p, const wg::Geometry& g) {
     if (p->path == WG_PATH_FUSED) return ok ? WG_PATH_FUSED : -1;
     if (p->path == WG_PATH_SEPARATE || !ok) return WG_PATH_SEPARATE;
     // fused for layers with many (tile, output channel) pairs and short rows;
-    // rows of up to 512 bytes when the output tile is at most 4 x 4 and there
-    // are 64 or more output channels (the fused kernel's unrolled instance)
+    // with the fused kernel's unrolled instance (output tile at most 4 x 4, 64
+    // or more output channels) rows of up to 512 bytes, from half as many pairs
     const int64_t row_bytes = g.Cp * wg::dtype_bytes(p->dtype);
-    const bool many = g.T * g.K >= (int64_t(1) << 20);
-    const bool rows = row_bytes <= 256 || (row_bytes <= 512 && g.m <= 4 && g.K >= 64);
-    return many && rows ? WG_PATH_FUSED : WG_PATH_SEPARATE;
+    const int64_t pairs = g.T * g.K;
+    const bool unrolled = g.m <= 4 && g.K >= 64;
+    const bool fused = (row_bytes <= 256 && pairs >= (int64_t(1) << 20)) ||
+                       (unrolled && row_bytes <= 512 && pairs >= (int64_t(1) << 19));
+    return fused ? WG_PATH_FUSED : WG_PATH_SEPARATE;
 }
 
 struct Layout {

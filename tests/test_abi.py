@@ -203,8 +203,10 @@ def test_conv_chunks_and_chunked_workspace():
         assert p.workspace_bytes(n, 224, 224, 64, 64) == u + v
     ps = Plan(WL.F4_A2P1, m=4, dtype="bf16", path="separate")
     assert ps.conv_chunks(32, 224, 224, 64, 64) == (1, 32)
-    assert p.conv_path(32, 28, 28, 512, 512) == "separate"
+    assert p.conv_path(32, 28, 28, 512, 512) == "separate"            # 1024-byte rows
     assert p.conv_chunks(32, 28, 28, 512, 512) == (1, 32)
+    assert p.conv_path(32, 28, 28, 256, 512) == "fused"               # 512-byte rows, 2^19 pairs and more
+    assert p.conv_path(8, 28, 28, 256, 512) == "separate"
 
 
 def test_conv_path_option_and_workspace():

@@ -108,7 +108,8 @@ def test_fused_matches_separate(spec, m, dtype):
 
 
 # VGG-16 layers that the automatic rule sends to the fused kernel (N = 1)
-VGG_FUSED = [(224, 3, 64), (224, 64, 64), (112, 64, 128), (112, 128, 128), (56, 128, 256), (56, 256, 256)]
+VGG_FUSED = [(224, 3, 64), (224, 64, 64), (112, 64, 128), (112, 128, 128), (56, 128, 256), (56, 256, 256),
+             (28, 256, 512)]
 
 
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
