@@ -14,8 +14,9 @@ ReLU and 2x2 max-pooling between layers (one HIP kernel each) run between the
 timed convolutions; the whole pass including them is reported too.
 
 Prints one JSON line: direct-equivalent TFLOP/s (2 N H W C K 9 flops per
-layer) from HIP events around each convolution (warm caches), the same with
-the caches flushed before every layer, per-layer and per-kernel durations,
+layer) from HIP events around each convolution (warm caches; a device fill
+before the first convolution keeps the GPU busy while the host enqueues it),
+the same with the caches flushed before every layer, per-layer and per-kernel durations,
 the roofline of the dominant (kernel, layer) launch, each layer's rel-L2
 error against float64 direct convolution, and the CPU oracle's throughput on
 a bounded sample of the same workload.
@@ -336,9 +337,11 @@ def run_vgg(a):
         stack.forward(x)
     torch.cuda.synchronize()
     per_layer = np.zeros(len(stack.layers))
+    lead = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device=x.device)   # 256 MiB, see timed_forward
     for _ in range(a.steps):
-        _, ms = stack.timed_forward(x)
+        _, ms = stack.timed_forward(x, lead=lead)
         per_layer += np.array(ms)
+    del lead
     per_layer /= a.steps
     ms_per_step = float(per_layer.sum())
     flops = stack.direct_flops(N)

@@ -67,13 +67,20 @@ class VggStack:
             x = relu_pool(y, L["pool"])
         return (x, trace) if keep else x
 
-    def timed_forward(self, x, flush=None):
+    def timed_forward(self, x, flush=None, lead=None):
         """One pass with HIP events around each convolution; returns (output,
         conv ms per layer).  With ``flush`` (a large device buffer) the buffer
         is overwritten before each convolution, outside its events, so that
-        each layer starts with its data out of the caches."""
+        each layer starts with its data out of the caches.  With ``lead`` (a
+        device buffer) the buffer is overwritten once before the first
+        convolution, outside its events: the GPU is then still busy while the
+        host enqueues that convolution, so its events time the GPU's work
+        rather than the host's launch latency (the later convolutions are
+        enqueued while earlier work runs)."""
         ev = []
         stream = torch.cuda.current_stream()
+        if lead is not None and flush is None:
+            lead.fill_(1)
         for L in self.layers:
             if flush is not None:
                 flush.fill_(1)
