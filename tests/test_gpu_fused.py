@@ -273,21 +273,24 @@ def test_unrolled_builtin_equals_runtime_coefficients(spec, m, dtype):
     assert torch.equal(yb, yr)
 
 
-@pytest.mark.parametrize("N", [9, 32])
-def test_conv2d_in_chunks_equals_one_launch(N):
-    """A batch whose V exceeds the chunk budget (224x224x64 -> 64, bf16: 19.7 MB
-    of V per image) runs as launch pairs over chunks of images (N = 9: 5 + 4,
-    N = 32: four of 8), with a workspace for one chunk's V; the output is the
-    fused kernel's over the whole batch, bit for bit."""
+@pytest.mark.parametrize("N,H,W,C,K,dtype", [(9, 224, 224, 64, 64, "bf16"), (32, 224, 224, 64, 64, "bf16"),
+                                              (9, 222, 222, 60, 70, "bf16"), (9, 222, 218, 60, 70, "f16")])
+def test_conv2d_in_chunks_equals_one_launch(N, H, W, C, K, dtype):
+    """A batch whose V exceeds the chunk budget (224x224x64 -> 64: 19.7 MB of V
+    per image in 16-bit) runs as launch pairs over chunks of images (N = 9:
+    5 + 4, N = 32: four of 8), with a workspace for one chunk's V; the output is
+    the fused kernel's over the whole batch, bit for bit.  The ragged cases
+    (a partial last tile row and column, C and K off the 64-channel blocks)
+    take the same split."""
     from paper_1905_05233_amd.winograd import Plan
-    H = W = 224
-    C = K = 64
-    x, w = _inputs((N, H, W, C, K), "bf16", seed=N)
-    p = Plan(WL.F4_A2P1, m=4, dtype="bf16")
+    x, w = _inputs((N, H, W, C, K), dtype, seed=N + C)
+    p = Plan(WL.F4_A2P1, m=4, dtype=dtype)
     assert p.conv_path(N, H, W, C, K) == "fused"
-    v_all = 49 * N * 56 * 56 * C * 2
+    n_chunks, chunk = p.conv_chunks(N, H, W, C, K)
+    assert n_chunks > 1 and chunk == -(-N // n_chunks)
+    v_all = 49 * N * (-(-H // 4)) * (-(-W // 4)) * (-(-C // 8) * 8) * 2
     assert p.workspace_bytes(N, H, W, C, K) < v_all        # one chunk's V, not the batch's
-    xd, wd = to_dev(x, "bf16"), to_dev(w, "bf16")
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
     y = p.conv2d(xd, wd)
     U, V = p.kernel_input_transform(wd, xd)
     y_one = p.contract_output(V, U, C, N, H, W)
