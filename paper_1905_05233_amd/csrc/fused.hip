@@ -545,9 +545,11 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_kernel(
 // C <= 32 in fp32; NSL = 2: twice that) and the block is 64 output channels x
 // 32 tiles (WT = 2), the contraction of a domain point is a single step of NSL
 // slices; rows of at most 64 bytes share one slice between XP = 128 / row
-// bytes domain points, as in the looped kernel's narrow steps; longer rows
-// (CH) take n_ch steps of two slices per domain point, in a loop at run time,
-// their MFMA chains accumulating over the steps.  This variant unrolls the
+// bytes domain points, as in the looped kernel's narrow steps; rows of three
+// or four slices take NCK = 2 steps of two slices per domain point, unrolled
+// like the rest; longer rows (CH) take n_ch steps of two slices per domain
+// point in a loop at run time.  In both, the MFMA chains of a domain point
+// accumulate over its steps.  This variant unrolls the
 // domain points at compile time: the
 // output-transform coefficients of every fold are constants (for a built-in
 // plan the zero terms disappear; for any other plan they are read from the
@@ -588,7 +590,7 @@ constexpr int groups_after(int s) {
     return issued - (s + 1);
 }
 
-template <int D, int MM, int ALPHA, class CO, int NSL, int XP, bool CH>
+template <int D, int MM, int ALPHA, class CO, int NSL, int XP, bool CH, int NCK>
 __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
     const unsigned char* __restrict__ V, const unsigned char* __restrict__ U, typename DTypeOf<D>::type* __restrict__ y,
     OutputTable tab, Geometry geo, int n_kb, int rb, int n_ch) {
@@ -596,10 +598,11 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
     using S = Storage<Elem>;
     constexpr int WT = 2;                  // two 16-tile blocks per wave
     constexpr int NPTS = ALPHA * ALPHA;    // domain points
-    constexpr int NSTEPS = (NPTS + XP - 1) / XP;
+    constexpr int NSTEPS = NCK * ((NPTS + XP - 1) / XP);
     constexpr int PPR = 8 / XP;            // 16-byte pieces of a domain point's row in a slice
     static_assert(XP == 1 || NSL == 1, "narrow rows fit one slice");
-    static_assert(!CH || (NSL == 2 && XP == 1), "long rows go in steps of two slices");
+    static_assert(!CH || (NSL == 2 && XP == 1 && NCK == 1), "long rows go in steps of two slices");
+    static_assert(NCK == 1 || (NSL == 2 && XP == 1 && !CH), "unrolled chunks are steps of two slices");
     constexpr int NST = unrolled_stages<NSL>();
     constexpr int kSB = unrolled_stage_bytes<NSL>();
     constexpr int kKD = 3 * NSL;           // DMA instructions per wave and step
@@ -671,7 +674,9 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
                       in ? roff[j] + (j < 2 ? pu : pv) : kOob);
             return;
         }
-        constexpr uint64_t xi = (s % ALPHA) * ALPHA + s / ALPHA;
+        // step s is chunk s % NCK (slices NSL (s % NCK) ..) of domain point s / NCK
+        constexpr int q = s / NCK, ck = s % NCK;
+        constexpr uint64_t xi = (q % ALPHA) * ALPHA + q / ALPHA;
         const auto ru = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(bu + xi * plane_u),
                                                           static_cast<short>(0), rec_u, static_cast<int>(kRsrcWord3));
         const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(bv + xi * plane_v),
@@ -679,11 +684,12 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
         unsigned char* st = lds + (s % NST) * kSB;
 #pragma unroll
         for (int sl = 0; sl < NSL; ++sl) {
-            const bool in = sl * kSlice + piece < rb;
+            constexpr int sb0 = ck * NSL * kSlice;
+            const bool in = sb0 + sl * kSlice + piece < rb;
 #pragma unroll
             for (int j = 0; j < 3; ++j)
                 dma16(j < 2 ? ru : rv, st + sl * kStageBytes + (wave + 4 * j) * 1024,
-                      in ? roff[j] + sl * kSlice : kOob);
+                      in ? roff[j] + sb0 + sl * kSlice : kOob);
         }
     };
 
@@ -796,16 +802,20 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
             });
             return;
         }
+        // NCK > 1: the first chunk of a domain point folds the previous one
+        constexpr int q = s / NCK, ck = s % NCK;
         u32x4 fa0 = lds_read16(cur + a_row + col0);
         u32x4 fa1 = lds_read16(cur + a_row + col1);
         u32x4 fb00 = lds_read16(cur + b_row + col0);
         u32x4 fb01 = lds_read16(cur + b_row + col1);
         u32x4 fb10 = lds_read16(cur + b_row + 16 * kSlice + col0);
         u32x4 fb11 = lds_read16(cur + b_row + 16 * kSlice + col1);
-        if constexpr (s > 0) fold(std::integral_constant<int, s - 1>{});
+        if constexpr (ck == 0 && q > 0) fold(std::integral_constant<int, q - 1>{});
         lds_settle(fa0, fa1, fb00, fb01, fb10, fb11);
-        part[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        part[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        if constexpr (ck == 0) {
+            part[0] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            part[1] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
         mma<D>(fa0, fb00, part[0]);
         mma<D>(fa0, fb10, part[1]);
         mma<D>(fa1, fb01, part[0]);
@@ -1085,16 +1095,17 @@ hipError_t launch_co_instance(const CoArgs& c, hipStream_t stream) {
 template <int D, int TT, int A, class CO>
 hipError_t launch_unrolled_instance(const CoArgs& c, hipStream_t stream) {
     using Elem = typename DTypeOf<D>::type;
-#define WG_UNR_LAUNCH(NSL, XP, CH)                                                                              \
-    hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, NSL, XP, CH>), dim3(c.nb),             \
+#define WG_UNR_LAUNCH(NSL, XP, CH, NCK)                                                                         \
+    hipLaunchKernelGGL((contract_output_unrolled_kernel<D, TT - 2, A, CO, NSL, XP, CH, NCK>), dim3(c.nb),        \
                        dim3(kThreads), 0, stream, c.V, c.U, static_cast<Elem*>(c.y), c.tab, c.g, c.n_kb, c.rb,   \
                        (c.n_slices + 1) / 2)
-    if (c.xp == 8) WG_UNR_LAUNCH(1, 8, false);
-    else if (c.xp == 4) WG_UNR_LAUNCH(1, 4, false);
-    else if (c.xp == 2) WG_UNR_LAUNCH(1, 2, false);
-    else if (c.n_slices == 1) WG_UNR_LAUNCH(1, 1, false);
-    else if (c.n_slices == 2) WG_UNR_LAUNCH(2, 1, false);
-    else WG_UNR_LAUNCH(2, 1, true);
+    if (c.xp == 8) WG_UNR_LAUNCH(1, 8, false, 1);
+    else if (c.xp == 4) WG_UNR_LAUNCH(1, 4, false, 1);
+    else if (c.xp == 2) WG_UNR_LAUNCH(1, 2, false, 1);
+    else if (c.n_slices == 1) WG_UNR_LAUNCH(1, 1, false, 1);
+    else if (c.n_slices == 2) WG_UNR_LAUNCH(2, 1, false, 1);
+    else if (c.n_slices <= 4) WG_UNR_LAUNCH(2, 1, false, 2);
+    else WG_UNR_LAUNCH(2, 1, true, 1);
 #undef WG_UNR_LAUNCH
     return hipGetLastError();
 }

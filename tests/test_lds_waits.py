@@ -287,28 +287,30 @@ def test_unrolled_kernels_wait_for_their_stage(fused_asm):
     the s-th group in issue order) must have completed, i.e. at least as many
     vector-memory operations were issued after the group's last load as the
     wait leaves outstanding.  The template arguments give alpha', the
-    slices per step and the domain points per step (steps = alpha'^2 / that,
-    rounded up)."""
+    slices per step, the domain points per step and the steps per domain
+    point (steps = alpha'^2 / the points per step, rounded up, times the
+    steps per point)."""
     for code, asm in fused_asm.items():
         body = asm[:asm.index("amdhsa.kernels")] if "amdhsa.kernels" in asm else asm
         parts = re.split(r"\n(_Z\S+):[^\n]*\n", body)
         seen = 0
         for i in range(1, len(parts), 2):
-            m = re.search(r"contract_output_unrolled_kernelILi\d+ELi\d+ELi(\d+)E.*ELi(\d)ELi(\d)ELb([01])EEEv",
+            m = re.search(r"contract_output_unrolled_kernelILi\d+ELi\d+ELi(\d+)E.*ELi(\d)ELi(\d)ELb([01])ELi(\d)EEEv",
                           parts[i])
             if not m:
                 continue
             seen += 1
             alpha, nsl, xp, ch = int(m.group(1)), int(m.group(2)), int(m.group(3)), m.group(4) == "1"
+            nck = int(m.group(5))
             if ch:
                 bad = chunked_wait_violations(parts[i + 1], 3 * nsl, 4 if nsl == 1 else 3)
                 assert not bad, f"dtype {code}: {parts[i][:80]}: {bad[:3]}"
                 continue
-            n = -(-alpha * alpha // xp)
+            n = -(-alpha * alpha // xp) * nck
             steps, bad = stage_wait_violations(parts[i + 1], 3 * nsl, n)
             assert steps == n, f"dtype {code}: {parts[i][:80]}: {steps} step barriers"
             assert not bad, f"dtype {code}: {parts[i][:80]}: stage loads not covered {bad[:3]}"
-        assert seen >= 48, f"dtype {code}: {seen} unrolled kernels"
+        assert seen >= 59, f"dtype {code}: {seen} unrolled kernels"
 
 
 def chunked_wait_violations(kernel_code, per_step, stages):
