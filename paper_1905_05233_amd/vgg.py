@@ -51,6 +51,20 @@ class VggStack:
             L["plan"] = Plan(spec.moduli, m=spec.m, dtype=dtype, inner=spec.inner)
             x = relu_pool(L["plan"].conv2d(x, L["w"]), L["pool"])
 
+    def share_workspace(self, N):
+        """Bind one device workspace, sized for the largest layer at batch N,
+        to every layer's plan.  The layers run one after another on one
+        stream, so they can share it; the next layer's transforms then write
+        where the previous layer's fused kernel read (a pass of the stack at
+        N = 32 in bf16: 1.89 against 1.92-1.96 ms with a workspace per layer)."""
+        if getattr(self, "_shared_n", None) == N:
+            return
+        need = max(L["plan"].workspace_bytes(N, L["hw"], L["hw"], L["C"], L["K"]) for L in self.layers)
+        ws = torch.empty(need, dtype=torch.uint8, device=self.layers[0]["w"].device)
+        for L in self.layers:
+            L["plan"].bind_workspace(ws)
+        self._shared_n = N
+
     def input(self, N, seed=0, device="cuda"):
         return torch.from_numpy(vgg_input(N, seed)).to(device).to(self.tdt)
 
@@ -60,6 +74,7 @@ class VggStack:
     def forward(self, x, keep=False):
         """Run the stack; with ``keep`` also return every layer's (input, raw conv output)."""
         trace = []
+        self.share_workspace(x.shape[0])
         for L in self.layers:
             y = L["plan"].conv2d(x, L["w"])
             if keep:
@@ -79,6 +94,7 @@ class VggStack:
         enqueued while earlier work runs)."""
         ev = []
         stream = torch.cuda.current_stream()
+        self.share_workspace(x.shape[0])
         if lead is not None and flush is None:
             lead.fill_(1)
         for L in self.layers:
