@@ -999,8 +999,12 @@ __global__ __launch_bounds__(kThreads, 2) void contract_output_unrolled_kernel(
                 }
                 const int hr = ty * MM + px / MM, wc = tx * MM + px % MM;
                 const int64_t ch = k0 + chunk * (16 / ES);
+                // non-temporal: y is written once and read by the next kernel, and
+                // as a streaming store it does not push out of L2 the U and V rows
+                // that the other blocks of this XCD are still reading
                 if (t0 + w * 16 + tl < T && hr < H && wc < W && ch < K)
-                    *reinterpret_cast<u32x4*>(ybytes + ((static_cast<int64_t>(n * H + hr) * W + wc) * K + ch) * ES) = v;
+                    __builtin_nontemporal_store(
+                        v, reinterpret_cast<u32x4*>(ybytes + ((static_cast<int64_t>(n * H + hr) * W + wc) * K + ch) * ES));
             }
         }
         return;
