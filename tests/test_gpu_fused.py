@@ -220,12 +220,16 @@ def test_unrolled_two_slices_matches_separate(spec, m, generic, dtype):
     _unrolled_vs_separate(spec, m, generic, dtype, slices=2)
 
 
-# long rows: two slices per step, the steps of a domain point in a loop
+# long rows: two slices per step; rows of three or four slices take two
+# unrolled steps per domain point, longer ones run the steps in a loop
 UNROLLED_LONG = [
     (WL.F4_A2P1, 4, False, "bf16", 256),     # 512-byte rows: 2 steps per domain point
+    (WL.F4_A2P1, 4, False, "f16", 256),      # the same in fp16
     (WL.F4_A2P1, 4, True, "f16", 200),       # 400-byte rows: the last step's second slice partly empty
     (WL.F2_LINEAR, 2, False, "f32", 100),    # 400-byte rows in fp32
-    ("0,a^2+1,a^2-2,inf", 4, False, "bf16", 520),   # 1040-byte rows: 5 steps, the last one's second slice empty
+    ("0,a^2+1,a^2-2,inf", 4, False, "bf16", 160),   # 320-byte rows: the second step's second slice empty
+    ("0,a^2+1,a^2-2,inf", 4, False, "bf16", 520),   # 1040-byte rows: 5 steps in a loop, the last one's second slice empty
+    (WL.F2_LINEAR, 2, True, "f32", 200),     # 800-byte rows: 4 steps in a loop, run-time coefficients
 ]
 
 
