@@ -32,6 +32,7 @@ namespace wg {
 namespace {
 
 constexpr int kBlock = 256;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // ----------------------------------------------------------------- kernel
 // U[xi = a*alpha + b][k][c] = sum_j (sum_i G[a][i] g[i][j]) G[b][j]; one thread
@@ -265,7 +266,12 @@ __device__ __forceinline__ void input_transform_unit(const InputTable& tab, cons
         const bool in = ci < P::kChunks && tile < geo.T && hr >= 0 && hr < geo.H && wc >= 0 && wc < geo.W;
         const Elem* src = x + ((static_cast<int64_t>(n) * geo.H + hr) * geo.W + wc) * geo.C + cc;
         if constexpr (kWhole) {
-            regs[p] = (in && cc < geo.C) ? *reinterpret_cast<const uint4*>(src) : uint4{0u, 0u, 0u, 0u};
+            // a streaming load: the layer input is read here and by no later
+            // kernel of the layer, so it is kept out of the last-level cache,
+            // which holds V for the contraction
+            const u32x4 t = (in && cc < geo.C) ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src))
+                                               : u32x4{0u, 0u, 0u, 0u};
+            regs[p] = uint4{t[0], t[1], t[2], t[3]};
         } else {
             Elem e[P::kChunkElems];
 #pragma unroll
