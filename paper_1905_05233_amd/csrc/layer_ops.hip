@@ -24,11 +24,16 @@ constexpr int kOpBlock = 256;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// 16 bytes to y as a non-temporal (streaming) store: the next layer's
-// transforms read y once, and a VGG-16 pass at N = 32 measured 1.78 against
-// 1.82 ms of convolution time with these outputs kept out of L2
+// 16 bytes as non-temporal (streaming) accesses: the input is read once and
+// the output is read once, by the next layer's transforms; kept out of the
+// caches, they leave the last-level cache to the next layer's V and U (a
+// VGG-16 pass at N = 32: 1.78 against 1.82 ms of convolution time for the
+// stores, 1.73 against 1.74 ms for the loads)
 __device__ __forceinline__ void store16_nt(void* dst, const void* src) {
     __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(src), reinterpret_cast<u32x4*>(dst));
+}
+__device__ __forceinline__ u32x4 load16_nt(const void* src) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
 }
 
 template <typename Elem>
@@ -47,7 +52,7 @@ __global__ __launch_bounds__(kOpBlock) void relu_kernel(const Elem* __restrict__
     if (i >= n) return;
     Elem e[VEC];
     if constexpr (VEC * sizeof(Elem) == 16) {
-        *reinterpret_cast<uint4*>(e) = *reinterpret_cast<const uint4*>(x + i);
+        *reinterpret_cast<u32x4*>(e) = load16_nt(x + i);
     } else {
 #pragma unroll
         for (int q = 0; q < VEC; ++q) e[q] = x[i + q];
@@ -84,7 +89,7 @@ __global__ __launch_bounds__(kOpBlock) void relu_pool_kernel(const Elem* __restr
             const Elem* src = x + ((n * H + 2 * i + di) * W + 2 * j + dj) * C + c;
             Elem e[VEC];
             if constexpr (VEC * sizeof(Elem) == 16) {
-                *reinterpret_cast<uint4*>(e) = *reinterpret_cast<const uint4*>(src);
+                *reinterpret_cast<u32x4*>(e) = load16_nt(src);
             } else {
 #pragma unroll
                 for (int q = 0; q < VEC; ++q) e[q] = src[q];
