@@ -99,6 +99,66 @@ __device__ __forceinline__ void kernel_transform_run(const KernelTable& tab, con
     }
 }
 
+// The same, one thread per (k, run of kRun channels) computing every row a:
+// the 3x3 taps are loaded once instead of once per row, and a launch needs
+// alpha' times fewer threads (the form the combined kernel/input launch uses,
+// so that fewer kernel-transform workgroups precede the input-transform ones).
+// Each output is computed in the same order as above.
+template <typename Elem, int ALPHA, int kRun, bool kWhole>
+__device__ __forceinline__ void kernel_transform_rows(const KernelTable& tab, const Elem* __restrict__ w,
+                                                      Elem* __restrict__ U, int64_t K, int64_t C, int64_t Cp,
+                                                      int64_t gid) {
+    using S = Storage<Elem>;
+    using Bits = typename RunBits<kRun * sizeof(Elem)>::type;
+    const int64_t runs = Cp / kRun;
+    if (gid >= K * runs) return;
+    const int64_t c = (gid % runs) * kRun;
+    const int64_t k = gid / runs;
+    const int64_t plane = K * Cp;
+    float g[3][3][kRun];
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            const Elem* src = w + ((k * 3 + i) * 3 + j) * C + c;
+            Elem e[kRun];
+            if constexpr (kWhole) {
+                *reinterpret_cast<Bits*>(e) = c < C ? *reinterpret_cast<const Bits*>(src) : Bits{};
+            } else {
+#pragma unroll
+                for (int q = 0; q < kRun; ++q) e[q] = c + q < C ? src[q] : S::from_f32(0.0f);
+            }
+#pragma unroll
+            for (int q = 0; q < kRun; ++q) g[i][j][q] = S::to_f32(e[q]);
+        }
+    Elem* out = U + k * Cp + c;
+#pragma unroll
+    for (int a = 0; a < ALPHA; ++a) {
+        float Gg[3][kRun];
+#pragma unroll
+        for (int j = 0; j < 3; ++j)
+#pragma unroll
+            for (int q = 0; q < kRun; ++q) {
+                float acc = 0.0f;
+#pragma unroll
+                for (int i = 0; i < 3; ++i) acc = __builtin_fmaf(tab.g[a * 3 + i], g[i][j][q], acc);
+                Gg[j][q] = acc;
+            }
+#pragma unroll
+        for (int b = 0; b < ALPHA; ++b) {
+            Elem e[kRun];
+#pragma unroll
+            for (int q = 0; q < kRun; ++q) {
+                float acc = 0.0f;
+#pragma unroll
+                for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(Gg[j][q], tab.g[b * 3 + j], acc);
+                e[q] = S::from_f32(acc);
+            }
+            *reinterpret_cast<Bits*>(out + (a * ALPHA + b) * plane) = *reinterpret_cast<const Bits*>(e);
+        }
+    }
+}
+
 template <typename Elem, int ALPHA, bool kWhole>
 __global__ __launch_bounds__(kBlock) void kernel_transform(KernelTable tab, const Elem* __restrict__ w,
                                                            Elem* __restrict__ U, int64_t K, int64_t C,
@@ -358,9 +418,10 @@ __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void input
 }
 
 // The kernel and input transforms are independent: conv2d runs them as one
-// launch.  The first n_kt workgroups each take P::kThreads runs of the kernel
-// transform, the rest are input-transform units (one launch instead of two,
-// and the short kernel transform overlaps the input transform).
+// launch.  The first n_kt workgroups each take P::kThreads (k, 4-channel run)
+// pairs of the kernel transform, every row a of each, the rest are
+// input-transform units (one launch instead of two, and the short kernel
+// transform overlaps the input transform).
 template <typename Elem, int TT, int ALPHA, bool kWhole, class CO, int PT>
 __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void kernel_input_transform(
     KernelTable ktab, InputTable itab, const Elem* __restrict__ w, const Elem* __restrict__ x,
@@ -368,7 +429,7 @@ __global__ __launch_bounds__((InputShape<Elem, TT, ALPHA>::kThreads)) void kerne
     using P = InputShape<Elem, TT, ALPHA>;
     const int64_t bid = blockIdx.x;
     if (bid < n_kt) {
-        kernel_transform_run<Elem, ALPHA, 4, kWhole>(ktab, w, U, geo.K, geo.C, geo.Cp, bid * P::kThreads + threadIdx.x);
+        kernel_transform_rows<Elem, ALPHA, 4, kWhole>(ktab, w, U, geo.K, geo.C, geo.Cp, bid * P::kThreads + threadIdx.x);
         return;
     }
     input_transform_unit<Elem, TT, ALPHA, kWhole, CO, PT>(itab, x, V, geo, bid - n_kt, gridDim.x - n_kt);
@@ -531,7 +592,7 @@ hipError_t launch_kit(const Geometry& g, const KernelTable& ktab, const InputTab
     constexpr bool kWalk = !__is_same(CO, RuntimeCoefs);   // as in launch_it
     const int pt = kWalk ? input_pt(g, whole) : 1;
     const int64_t units = input_units(g, pt);
-    const int64_t kt_runs = static_cast<int64_t>(g.alpha) * g.K * (g.Cp / 4);
+    const int64_t kt_runs = g.K * (g.Cp / 4);   // one thread per (k, 4-channel run), every row a
     // a multiple of 8, so the input transform's ids keep their XCD (id mod 8)
     const int64_t n_kt = (kt_runs + 8 * kThr - 1) / (8 * kThr) * 8;
     if (n_kt + units > 0x7fffffff) return hipErrorInvalidValue;
